@@ -1,0 +1,11 @@
+// 4-bit instantiations of the MFMA implicit-GEMM convolution.
+#include "conv_mfma_impl.h"
+
+namespace qnn {
+
+hipError_t launch_conv_mfma_b4(const ConvArgs &a, int mr, int nc, int al16, dim3 grid, hipStream_t s)
+{
+    return launch_conv_mfma_bits<4>(a, mr, nc, al16, grid, s);
+}
+
+}  // namespace qnn

@@ -1,0 +1,212 @@
+// INT-1 (binary) convolution by XNOR and population count (Sec. III-A,
+// Eq. (5); Sec. IV-A "Binary Convolution Kernel").
+//
+// Each lane owns one output pixel.  General form (any filter volume): the
+// lane walks its receptive field one packed 32-channel word at a time and,
+// for 32 output channels at once, adds popcount(~(x ^ w)) to 32 counters.  The filter words are the
+// same for every lane of a wave, so they are fetched by scalar loads and fed
+// to v_xnor_b32 / v_bcnt_u32_b32 as scalar operands: two vector instructions
+// per 32 binary MACs.  Padding taps hold bit 0 (value -1).  The +-1 dot
+// product is 2 * popcount - K; the output bit of channel m is
+// (dot + bias[m] >= thresh[m]), 32 channels packed per output word.
+#include "qnn_internal.h"
+
+namespace qnn {
+
+template <int KB>
+__global__ void __launch_bounds__(256) conv_xnor_kernel(const uint32_t *__restrict__ xg,
+                                                        const uint32_t *__restrict__ wgl, XnorArgs a)
+{
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    const bool live = p < a.npix;
+    const int pc = live ? p : a.npix - 1;
+    const int q = (int)fdiv((uint32_t)pc, a.div_wo);
+    const int ox = pc - q * a.wo;
+    const int n = (int)fdiv((uint32_t)q, a.div_ho);
+    const int oy = q - n * a.ho;
+    const int ngroups = (a.m + 31) >> 5;
+
+    for (int grp = 0; grp < ngroups; ++grp) {
+        uint32_t pop[32];
+#pragma unroll
+        for (int i = 0; i < 32; ++i)
+            pop[i] = 0;
+        const uint32_t *wg = wgl + grp * 32 * a.kd;
+        const int nvalid = min(32, a.m - grp * 32);
+        for (int ky = 0; ky < a.kh; ++ky) {
+            const int iy = oy * a.sh - a.ph + ky;
+            for (int kx = 0; kx < a.kw; ++kx) {
+                const int ix = ox * a.sw - a.pw + kx;
+                const bool in = iy >= 0 && iy < a.h && ix >= 0 && ix < a.w_;
+                const uint32_t *xp = xg + ((n * a.h + (in ? iy : 0)) * a.w_ + (in ? ix : 0)) * a.cd;
+                const uint32_t *wt = wg + (ky * a.kw + kx) * a.cd;
+                for (int d0 = 0; d0 < a.cd; d0 += KB) {
+                    uint32_t xv[KB];
+#pragma unroll
+                    for (int d = 0; d < KB; ++d)
+                        xv[d] = in ? xp[d0 + d] : 0u;
+                    if (nvalid == 32) {
+#pragma unroll
+                        for (int mm = 0; mm < 32; ++mm)
+#pragma unroll
+                            for (int d = 0; d < KB; ++d)
+                                pop[mm] += __popc(~(xv[d] ^ wt[mm * a.kd + d0 + d]));
+                    } else {
+#pragma unroll
+                        for (int mm = 0; mm < 32; ++mm) {
+                            if (mm < nvalid) {
+#pragma unroll
+                                for (int d = 0; d < KB; ++d)
+                                    pop[mm] += __popc(~(xv[d] ^ wt[mm * a.kd + d0 + d]));
+                            }
+                        }
+                    }
+                }
+            }
+        }
+        if (!live)
+            continue;
+        if (a.epi == EPI_RAW32) {
+            int32_t *yr = (int32_t *)a.y + (size_t)p * a.m + grp * 32;
+            for (int mm = 0; mm < nvalid; ++mm) {
+                int64_t dot = 2 * (int64_t)pop[mm] - a.kbits;
+                int64_t v = dot + (a.bias ? a.bias[grp * 32 + mm] : 0);
+                yr[mm] = (int32_t)(uint32_t)(uint64_t)v;
+            }
+        } else {
+            uint32_t word = 0;
+#pragma unroll
+            for (int mm = 0; mm < 32; ++mm) {
+                if (mm < nvalid) {
+                    const int m = grp * 32 + mm;
+                    int64_t dot = 2 * (int64_t)pop[mm] - a.kbits;
+                    int64_t v = dot + (a.bias ? a.bias[m] : 0);
+                    word |= (v >= a.thresh[m] ? 1u : 0u) << mm;
+                }
+            }
+            uint8_t *yb = a.y + (size_t)p * a.ypb + grp * 4;
+            const int nb = min(4, a.ypb - grp * 4);
+            if (nb == 4 && (a.ypb & 3) == 0) {
+                *(uint32_t *)yb = word;
+            } else {
+                for (int b = 0; b < nb; ++b)
+                    yb[b] = (uint8_t)(word >> (8 * b));
+            }
+        }
+    }
+}
+
+// Register-resident variant (kd a multiple of 8): a lane gathers its whole
+// im2col column (kd <= KDM words, zero bits for padding taps) once, then loops over the output
+// channels; channel m's kd filter words are loaded by scalar loads and used
+// as scalar operands.  Only one channel's words are live at a time.
+template <int KDM>
+__global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__restrict__ xg,
+                                                            const uint32_t *__restrict__ wgl,
+                                                            const int32_t *__restrict__ bias,
+                                                            const int32_t *__restrict__ thresh,
+                                                            XnorArgs a)
+{
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    const bool live = p < a.npix;
+    const int pc = live ? p : a.npix - 1;
+    const int q = (int)fdiv((uint32_t)pc, a.div_wo);
+    const int ox = pc - q * a.wo;
+    const int n = (int)fdiv((uint32_t)q, a.div_ho);
+    const int oy = q - n * a.ho;
+
+    uint32_t xv[KDM];
+#pragma unroll
+    for (int k = 0; k < KDM; ++k) {
+        xv[k] = 0u;
+        if (k < a.kd) {
+            const int tap = (int)fdiv((uint32_t)k, a.div_cd);
+            const int d = k - tap * a.cd;
+            const int ky = (int)fdiv((uint32_t)tap, a.div_kw);
+            const int kx = tap - ky * a.kw;
+            const int iy = oy * a.sh - a.ph + ky, ix = ox * a.sw - a.pw + kx;
+            if (iy >= 0 && iy < a.h && ix >= 0 && ix < a.w_)
+                xv[k] = xg[((n * a.h + iy) * a.w_ + ix) * a.cd + d];
+        }
+    }
+
+    uint32_t word = 0;
+    for (int m = 0; m < a.m; ++m) {
+        // kd is a multiple of 8: the filter row is walked in 32-byte blocks;
+        // block b + 1 is fetched while block b is consumed, and the
+        // scheduling barriers keep the compiler from hoisting every block's
+        // scalar loads (which would spill scalar registers).
+        const uint4 *wr = (const uint4 *)(wgl + m * a.kd);
+        uint4 c0 = wr[0], c1 = wr[1];
+        uint32_t pop = 0;
+#pragma unroll
+        for (int kb = 0; kb < KDM; kb += 8) {
+            if (kb < a.kd) {
+                uint4 n0 = c0, n1 = c1;
+                if (kb + 8 < a.kd) {
+                    n0 = wr[(kb + 8) / 4];
+                    n1 = wr[(kb + 8) / 4 + 1];
+                }
+                pop += __popc(~(xv[kb + 0] ^ c0.x));
+                pop += __popc(~(xv[kb + 1] ^ c0.y));
+                pop += __popc(~(xv[kb + 2] ^ c0.z));
+                pop += __popc(~(xv[kb + 3] ^ c0.w));
+                pop += __popc(~(xv[kb + 4] ^ c1.x));
+                pop += __popc(~(xv[kb + 5] ^ c1.y));
+                pop += __popc(~(xv[kb + 6] ^ c1.z));
+                pop += __popc(~(xv[kb + 7] ^ c1.w));
+                c0 = n0;
+                c1 = n1;
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        const int64_t v = 2 * (int64_t)pop - a.kbits + (bias ? bias[m] : 0);
+        if (a.epi == EPI_RAW32) {
+            if (live)
+                ((int32_t *)a.y)[(size_t)p * a.m + m] = (int32_t)(uint32_t)(uint64_t)v;
+            continue;
+        }
+        word |= (v >= thresh[m] ? 1u : 0u) << (m & 31);
+        if ((m & 31) == 31 || m == a.m - 1) {
+            if (live) {
+                uint8_t *yb = a.y + (size_t)p * a.ypb + (m >> 5) * 4;
+                const int nb = min(4, a.ypb - (m >> 5) * 4);
+                if (nb == 4 && (a.ypb & 3) == 0) {
+                    *(uint32_t *)yb = word;
+                } else {
+                    for (int b = 0; b < nb; ++b)
+                        yb[b] = (uint8_t)(word >> (8 * b));
+                }
+            }
+            word = 0;
+        }
+    }
+}
+
+hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s)
+{
+    dim3 grid((a.npix + 255) / 256);
+    if (a.kd % 8 != 0 || a.kd > 128)
+        ;
+    else if (a.kd <= 32)
+        hipLaunchKernelGGL(conv_xnor_res_kernel<32>, grid, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
+    else if (a.kd <= 64)
+        hipLaunchKernelGGL(conv_xnor_res_kernel<64>, grid, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
+    else if (a.kd <= 96)
+        hipLaunchKernelGGL(conv_xnor_res_kernel<96>, grid, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
+    else
+        hipLaunchKernelGGL(conv_xnor_res_kernel<128>, grid, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
+    if (a.kd % 8 == 0 && a.kd <= 128)
+        return hipGetLastError();
+    if (a.cd % 8 == 0)
+        hipLaunchKernelGGL(conv_xnor_kernel<8>, grid, dim3(256), 0, s, a.x, a.w, a);
+    else if (a.cd % 4 == 0)
+        hipLaunchKernelGGL(conv_xnor_kernel<4>, grid, dim3(256), 0, s, a.x, a.w, a);
+    else if (a.cd % 2 == 0)
+        hipLaunchKernelGGL(conv_xnor_kernel<2>, grid, dim3(256), 0, s, a.x, a.w, a);
+    else
+        hipLaunchKernelGGL(conv_xnor_kernel<1>, grid, dim3(256), 0, s, a.x, a.w, a);
+    return hipGetLastError();
+}
+
+}  // namespace qnn

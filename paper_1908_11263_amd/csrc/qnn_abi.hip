@@ -1,0 +1,536 @@
+// C ABI of the quantized-convolution library: argument validation (entirely
+// on the host, before any device call), tile planning and kernel dispatch.
+#include <mutex>
+#include <string.h>
+
+#include "qnn.h"
+#include "qnn_internal.h"
+
+using namespace qnn;
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+constexpr int kLdsBytes = 160 * 1024;
+
+struct DeviceInfo {
+    int checked = 0;  // 0 unknown, 1 ok, -1 not usable
+    int cus = 0;
+};
+
+std::mutex g_mu;
+DeviceInfo g_dev[kMaxDevices];
+
+qnn_status device_info(int *cus)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return QNN_ERR_DEVICE;
+    std::lock_guard<std::mutex> lock(g_mu);
+    DeviceInfo &d = g_dev[dev];
+    if (d.checked == 0) {
+        hipDeviceProp_t prop;
+        if (hipGetDeviceProperties(&prop, dev) != hipSuccess) {
+            d.checked = -1;
+        } else {
+            d.checked = strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : -1;
+            d.cus = prop.multiProcessorCount;
+        }
+    }
+    if (d.checked != 1)
+        return QNN_ERR_DEVICE;
+    if (cus)
+        *cus = d.cus;
+    return QNN_OK;
+}
+
+bool valid_bits(int b) { return b == 1 || b == 2 || b == 4 || b == 8; }
+
+int64_t pixel_bytes64(const qnn_tensor *t)
+{
+    if (t->bits == 32)
+        return 4 * (int64_t)t->c;
+    return ((int64_t)t->c * t->bits + 7) / 8;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+int32_t out_dim(int32_t in, int32_t k, int32_t s, int32_t p)
+{
+    int64_t span = (int64_t)in + 2 * (int64_t)p - k;
+    if (span < 0)
+        return 0;
+    return (int32_t)(span / s + 1);
+}
+
+int out_bits_for(int32_t kind, int32_t in_bits)
+{
+    if (kind == QNN_EPI_REQUANT)
+        return in_bits;
+    if (kind == QNN_EPI_THRESH1)
+        return 1;
+    return 32;
+}
+
+int64_t max_k_for(int bits)
+{
+    // K * max|x'| * max|w'| < 2^31 on the accumulator the kernels keep, and
+    // K * max|x| * max|w| < 2^31 for the true accumulator.
+    switch (bits) {
+    case 8: return 65793;     // 255 * 128 * K < 2^31 (true); 128 * 128 * K < 2^31 (offset form)
+    case 4: return 1118481;   // 15 * 128 * K < 2^31 (weights staged as 16 * w)
+    case 2: return 5592405;   // 3 * 128 * K < 2^31 (weights staged as 64 * w)
+    default: return 2147483647;
+    }
+}
+
+qnn_status check_tensor(const qnn_tensor *t)
+{
+    if (t->n < 0 || t->h < 1 || t->w < 1 || t->c < 1)
+        return QNN_ERR_SHAPE;
+    if ((int64_t)t->n * t->h * t->w * pixel_bytes64(t) > ((int64_t)1 << 40))
+        return QNN_ERR_SHAPE;
+    return QNN_OK;
+}
+
+qnn_status check_epi(const qnn_epi *e, int bits, int32_t m)
+{
+    (void)m;
+    switch (e->kind) {
+    case QNN_EPI_REQUANT:
+        if (bits == 1)
+            return QNN_ERR_BITS;
+        if (!e->mult || !e->shift)
+            return QNN_ERR_NULL;
+        if (e->clip_lo < 0 || e->clip_lo > e->clip_hi || e->clip_hi > (1 << bits) - 1)
+            return QNN_ERR_PARAM;
+        break;
+    case QNN_EPI_THRESH1:
+        if (bits != 1)
+            return QNN_ERR_BITS;
+        if (!e->thresh)
+            return QNN_ERR_NULL;
+        break;
+    case QNN_EPI_RAW32:
+        break;
+    default:
+        return QNN_ERR_PARAM;
+    }
+    return QNN_OK;
+}
+
+// Tile planning for the MFMA convolution.  Returns QNN_ERR_UNSUPPORTED when no
+// tile fits the local memory of a compute unit.
+qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
+{
+    const int c8 = a.c8;
+    a.row_mode = (c8 % 16) != 0;
+    int kchunks, ps;
+    if (a.row_mode) {
+        a.row_len = a.kw * c8;
+        a.cpr = (a.row_len + 15) / 16;
+        kchunks = a.kh * a.cpr;
+        ps = c8;
+    } else {
+        a.row_len = 0;
+        a.cpr = 0;
+        kchunks = a.kh * a.kw * (c8 / 16);
+        // keep the pixel stride an odd multiple of 16 bytes, so 16 lanes
+        // reading 16 neighbouring pixels hit 16 different bank groups
+        ps = ((c8 / 16) % 2 == 0) ? c8 + 16 : c8;
+    }
+    a.kchunks = kchunks;
+    a.ksteps = (kchunks + 3) / 4;
+    a.kp = a.ksteps * 64 + 16;
+    a.ps = ps;
+    al16 = a.row_mode ? 0 : 1;
+    const int obits = a.epi == EPI_REQUANT ? bits : 32;
+    const int64_t tab_bytes = 3 * 4 * (int64_t)(4 * a.ksteps);
+
+    int mr_first = a.m <= 16 ? 1 : (a.m <= 32 ? 2 : 4);
+    for (mr = mr_first; mr >= 1; mr >>= 1) {
+        for (nc = 4; nc >= 1; nc >>= 1) {
+            const int MT = 16 * mr, PT = 64 * nc;
+            int ti, th, tw;
+            if ((int64_t)a.ho * a.wo >= PT) {
+                ti = 1;
+                tw = a.wo < PT ? a.wo : PT;
+                th = PT / tw;
+                if (th > a.ho)
+                    th = a.ho;
+            } else {
+                ti = PT / (a.ho * a.wo);
+                if (ti > a.n)
+                    ti = a.n > 0 ? a.n : 1;
+                th = a.ho;
+                tw = a.wo;
+            }
+            const int hh = (th - 1) * a.sh + a.kh;
+            const int hwd = (tw - 1) * a.sw + a.kw;
+            const int64_t w_bytes = (int64_t)MT * a.kp;
+            const int64_t x_bytes = (int64_t)ti * hh * hwd * ps + 64;
+            const int ot_b = obits == 32 ? 0 : MT * bits / 8;
+            const int64_t o_bytes = (int64_t)PT * ot_b;
+            int64_t off = w_bytes;
+            const int64_t off_tab = off;
+            off += tab_bytes;
+            const int64_t off_wsum = off;
+            off += 4 * MT;
+            off = (off + 15) & ~(int64_t)15;
+            const int64_t off_x = off;
+            off += (x_bytes + 15) & ~(int64_t)15;
+            const int64_t off_out = off;
+            off += o_bytes;
+            if (off > kLdsBytes)
+                continue;
+            a.ti = ti;
+            a.th = th;
+            a.tw = tw;
+            a.hh = hh;
+            a.hwd = hwd;
+            a.ot_b = ot_b;
+            a.off_tab = (int32_t)off_tab;
+            a.off_wsum = (int32_t)off_wsum;
+            a.off_x = (int32_t)off_x;
+            a.off_out = (int32_t)off_out;
+            a.lds_bytes = (int32_t)off;
+            a.tiles_x = (a.wo + tw - 1) / tw;
+            a.tiles_y = (a.ho + th - 1) / th;
+            const int64_t tiles_n = (a.n + ti - 1) / ti;
+            const int64_t nt = tiles_n * a.tiles_y * a.tiles_x;
+            if (nt > (int64_t)1 << 30)
+                return QNN_ERR_UNSUPPORTED;
+            a.ntiles = (int32_t)nt;
+            return QNN_OK;
+        }
+    }
+    return QNN_ERR_UNSUPPORTED;
+}
+
+qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
+                    const qnn_conv_geom *g, const qnn_epi *e, const qnn_tensor *y, void *y_dev,
+                    void *stream)
+{
+    if (!x || !g || !e || !y)
+        return QNN_ERR_NULL;
+    if (!valid_bits(x->bits))
+        return QNN_ERR_BITS;
+    qnn_status st = check_tensor(x);
+    if (st != QNN_OK)
+        return st;
+    if (m < 1)
+        return QNN_ERR_SHAPE;
+    if (g->kh < 1 || g->kw < 1 || g->stride_h < 1 || g->stride_w < 1 || g->pad_h < 0 ||
+        g->pad_w < 0 || g->pad_h > 1024 || g->pad_w > 1024 || g->kh > 4096 || g->kw > 4096)
+        return QNN_ERR_PARAM;
+    st = check_epi(e, x->bits, m);
+    if (st != QNN_OK)
+        return st;
+    const int obits = out_bits_for(e->kind, x->bits);
+    const int32_t ho = out_dim(x->h, g->kh, g->stride_h, g->pad_h);
+    const int32_t wo = out_dim(x->w, g->kw, g->stride_w, g->pad_w);
+    if (ho < 1 || wo < 1)
+        return QNN_ERR_SHAPE;
+    if (y->n != x->n || y->h != ho || y->w != wo || y->c != m)
+        return QNN_ERR_SHAPE;
+    if (y->bits != obits)
+        return QNN_ERR_BITS;
+    const int64_t pb = pixel_bytes64(x);
+    if ((int64_t)x->c * x->bits % 32 != 0)
+        return QNN_ERR_ALIGN;
+    const int64_t K = (int64_t)g->kh * g->kw * x->c;
+    if (K > max_k_for(x->bits))
+        return QNN_ERR_OVERFLOW;
+    if ((int64_t)x->n * ho * wo >= ((int64_t)1 << 31) || (int64_t)x->n * x->h * x->w >= ((int64_t)1 << 31))
+        return QNN_ERR_SHAPE;
+    if (x->n == 0)
+        return QNN_OK;
+    if (!x_dev || !w_dev || !y_dev)
+        return QNN_ERR_NULL;
+    if (!aligned16(x_dev) || !aligned16(w_dev) || !aligned16(y_dev))
+        return QNN_ERR_ALIGN;
+    hipStream_t s = (hipStream_t)stream;
+    const int ypb = (int)pixel_bytes64(y);
+    int cus = 0;
+
+    if (x->bits == 1) {
+        st = device_info(&cus);
+        if (st != QNN_OK)
+            return st;
+        XnorArgs a;
+        memset(&a, 0, sizeof(a));
+        a.x = (const uint32_t *)x_dev;
+        a.w = (const uint32_t *)w_dev;
+        a.y = (uint8_t *)y_dev;
+        a.bias = e->bias;
+        a.thresh = e->thresh;
+        a.n = x->n; a.h = x->h; a.w_ = x->w; a.cd = (int32_t)(pb / 4);
+        a.m = m; a.kh = g->kh; a.kw = g->kw; a.sh = g->stride_h; a.sw = g->stride_w;
+        a.ph = g->pad_h; a.pw = g->pad_w; a.ho = ho; a.wo = wo;
+        a.kd = g->kh * g->kw * a.cd;
+        a.kbits = (int32_t)K;
+        a.epi = e->kind;
+        a.ypb = ypb;
+        a.npix = x->n * ho * wo;
+        a.div_wo = make_fastdiv((uint32_t)wo);
+        a.div_ho = make_fastdiv((uint32_t)ho);
+        a.div_cd = make_fastdiv((uint32_t)a.cd);
+        a.div_kw = make_fastdiv((uint32_t)a.kw);
+        return launch_conv_xnor(a, s) == hipSuccess ? QNN_OK : QNN_ERR_LAUNCH;
+    }
+
+    ConvArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = (const uint8_t *)x_dev;
+    a.w = (const uint8_t *)w_dev;
+    a.y = (uint8_t *)y_dev;
+    a.bias = e->bias;
+    a.mult = e->mult;
+    a.shift = e->shift;
+    a.n = x->n; a.h = x->h; a.w_ = x->w; a.pb = (int32_t)pb; a.c8 = x->c;
+    a.m = m; a.kh = g->kh; a.kw = g->kw; a.sh = g->stride_h; a.sw = g->stride_w;
+    a.ph = g->pad_h; a.pw = g->pad_w; a.ho = ho; a.wo = wo;
+    a.wrow = (int32_t)(K * x->bits / 8);
+    a.epi = e->kind;
+    a.clip_lo = e->clip_lo;
+    a.clip_hi = e->clip_hi;
+    a.ypb = ypb;
+    int mr, nc, al16;
+    st = plan_conv_mfma(a, x->bits, mr, nc, al16);
+    if (st != QNN_OK)
+        return st;
+    a.quad16 = (pb % 16) == 0;
+    a.pbq = (int32_t)(a.quad16 ? pb / 16 : pb / 4);
+    a.div_pbq = make_fastdiv((uint32_t)a.pbq);
+    a.div_hwd = make_fastdiv((uint32_t)a.hwd);
+    a.div_hh = make_fastdiv((uint32_t)a.hh);
+    a.div_tile_px = make_fastdiv((uint32_t)(a.th * a.tw));
+    a.div_tw = make_fastdiv((uint32_t)a.tw);
+    a.div_tx = make_fastdiv((uint32_t)a.tiles_x);
+    a.div_ty = make_fastdiv((uint32_t)a.tiles_y);
+    if (a.epi == EPI_REQUANT) {
+        a.oquad16 = (ypb % 4) == 0;   // copy whole 4-byte words when every tile's range is word-sized
+        a.obq = a.oquad16 ? a.ot_b / 4 : a.ot_b;
+    } else {
+        a.oquad16 = 0;
+        a.obq = 1;
+    }
+    a.div_obq = make_fastdiv((uint32_t)a.obq);
+    st = device_info(&cus);
+    if (st != QNN_OK)
+        return st;
+    const int MT = 16 * mr;
+    const int mtiles = (m + MT - 1) / MT;
+    const int per_cu = a.lds_bytes * 2 <= kLdsBytes ? 2 : 1;
+    int64_t gx = (int64_t)cus * per_cu;
+    if (gx > a.ntiles)
+        gx = a.ntiles;
+    if (gx < 1)
+        gx = 1;
+    dim3 grid((unsigned)gx, (unsigned)mtiles);
+    hipError_t err;
+    if (x->bits == 8)
+        err = launch_conv_mfma_b8(a, mr, nc, al16, grid, s);
+    else if (x->bits == 4)
+        err = launch_conv_mfma_b4(a, mr, nc, al16, grid, s);
+    else
+        err = launch_conv_mfma_b2(a, mr, nc, al16, grid, s);
+    return err == hipSuccess ? QNN_OK : QNN_ERR_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t qnn_abi_version(void) { return QNN_ABI_VERSION; }
+
+const char *qnn_status_string(qnn_status s)
+{
+    switch (s) {
+    case QNN_OK: return "ok";
+    case QNN_ERR_NULL: return "a required pointer is NULL";
+    case QNN_ERR_BITS: return "unsupported or mismatched bit-width";
+    case QNN_ERR_SHAPE: return "invalid or inconsistent tensor shape";
+    case QNN_ERR_PARAM: return "parameter out of range";
+    case QNN_ERR_ALIGN: return "pixel bytes not a multiple of 4 or device pointer not 16-byte aligned";
+    case QNN_ERR_OVERFLOW: return "filter volume too large for the 32-bit accumulator";
+    case QNN_ERR_UNSUPPORTED: return "shape exceeds the kernels' local-memory limits";
+    case QNN_ERR_DEVICE: return "no usable gfx950 device is current";
+    case QNN_ERR_LAUNCH: return "kernel launch failed";
+    }
+    return "unknown status";
+}
+
+qnn_status qnn_device_check(void) { return device_info(nullptr); }
+
+size_t qnn_pixel_bytes(const qnn_tensor *t)
+{
+    if (!t || t->c < 0)
+        return 0;
+    return (size_t)pixel_bytes64(t);
+}
+
+size_t qnn_tensor_bytes(const qnn_tensor *t)
+{
+    if (!t || t->n < 0 || t->h < 0 || t->w < 0 || t->c < 0)
+        return 0;
+    return (size_t)t->n * t->h * t->w * (size_t)pixel_bytes64(t);
+}
+
+qnn_status qnn_conv2d_out_shape(const qnn_tensor *x, int32_t m, const qnn_conv_geom *g,
+                                int32_t kind, qnn_tensor *y)
+{
+    if (!x || !g || !y)
+        return QNN_ERR_NULL;
+    if (!valid_bits(x->bits))
+        return QNN_ERR_BITS;
+    if (check_tensor(x) != QNN_OK || m < 1)
+        return QNN_ERR_SHAPE;
+    if (g->kh < 1 || g->kw < 1 || g->stride_h < 1 || g->stride_w < 1 || g->pad_h < 0 || g->pad_w < 0)
+        return QNN_ERR_PARAM;
+    if (kind != QNN_EPI_REQUANT && kind != QNN_EPI_THRESH1 && kind != QNN_EPI_RAW32)
+        return QNN_ERR_PARAM;
+    if ((kind == QNN_EPI_REQUANT && x->bits == 1) || (kind == QNN_EPI_THRESH1 && x->bits != 1))
+        return QNN_ERR_BITS;
+    const int32_t ho = out_dim(x->h, g->kh, g->stride_h, g->pad_h);
+    const int32_t wo = out_dim(x->w, g->kw, g->stride_w, g->pad_w);
+    if (ho < 1 || wo < 1)
+        return QNN_ERR_SHAPE;
+    y->n = x->n;
+    y->h = ho;
+    y->w = wo;
+    y->c = m;
+    y->bits = out_bits_for(kind, x->bits);
+    return QNN_OK;
+}
+
+qnn_status qnn_conv2d(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
+                      const qnn_conv_geom *g, const qnn_epi *e, const qnn_tensor *y, void *y_dev,
+                      void *stream)
+{
+    return run_conv(x, x_dev, m, w_dev, g, e, y, y_dev, stream);
+}
+
+qnn_status qnn_linear(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
+                      const qnn_epi *e, const qnn_tensor *y, void *y_dev, void *stream)
+{
+    if (!x || !e || !y)
+        return QNN_ERR_NULL;
+    if (y->h != 1 || y->w != 1)
+        return QNN_ERR_SHAPE;
+    qnn_conv_geom g = {x->h, x->w, 1, 1, 0, 0};
+    return run_conv(x, x_dev, m, w_dev, &g, e, y, y_dev, stream);
+}
+
+qnn_status qnn_maxpool2d(const qnn_tensor *x, const void *x_dev, int32_t kh, int32_t kw,
+                         int32_t sh, int32_t sw, const qnn_tensor *y, void *y_dev, void *stream)
+{
+    if (!x || !y)
+        return QNN_ERR_NULL;
+    if (x->bits != 8 && x->bits != 4 && x->bits != 2)
+        return QNN_ERR_BITS;
+    qnn_status st = check_tensor(x);
+    if (st != QNN_OK)
+        return st;
+    if (kh < 1 || kw < 1 || sh < 1 || sw < 1)
+        return QNN_ERR_PARAM;
+    const int32_t ho = out_dim(x->h, kh, sh, 0), wo = out_dim(x->w, kw, sw, 0);
+    if (ho < 1 || wo < 1)
+        return QNN_ERR_SHAPE;
+    if (y->n != x->n || y->h != ho || y->w != wo || y->c != x->c)
+        return QNN_ERR_SHAPE;
+    if (y->bits != x->bits)
+        return QNN_ERR_BITS;
+    const int64_t pb = pixel_bytes64(x);
+    if ((int64_t)x->c * x->bits % 32 != 0)
+        return QNN_ERR_ALIGN;
+    const int64_t total = (int64_t)x->n * ho * wo * (pb / 4);
+    if (total >= ((int64_t)1 << 31) || (int64_t)x->n * x->h * x->w >= ((int64_t)1 << 31))
+        return QNN_ERR_SHAPE;
+    if (x->n == 0)
+        return QNN_OK;
+    if (!x_dev || !y_dev)
+        return QNN_ERR_NULL;
+    if (!aligned16(x_dev) || !aligned16(y_dev))
+        return QNN_ERR_ALIGN;
+    st = device_info(nullptr);
+    if (st != QNN_OK)
+        return st;
+    PoolArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = (const uint8_t *)x_dev;
+    a.y = (uint8_t *)y_dev;
+    a.n = x->n; a.h = x->h; a.w_ = x->w; a.pbd = (int32_t)(pb / 4);
+    a.kh = kh; a.kw = kw; a.sh = sh; a.sw = sw; a.ho = ho; a.wo = wo;
+    a.total = (int32_t)total;
+    a.div_pbd = make_fastdiv((uint32_t)a.pbd);
+    a.div_wo = make_fastdiv((uint32_t)wo);
+    a.div_ho = make_fastdiv((uint32_t)ho);
+    return launch_maxpool(a, x->bits, (hipStream_t)stream) == hipSuccess ? QNN_OK : QNN_ERR_LAUNCH;
+}
+
+qnn_status qnn_relu_s8(const void *x_dev, void *y_dev, size_t count, void *stream)
+{
+    if (count == 0)
+        return QNN_OK;
+    if (!x_dev || !y_dev)
+        return QNN_ERR_NULL;
+    if (!aligned16(x_dev) || !aligned16(y_dev))
+        return QNN_ERR_ALIGN;
+    if (count >= ((size_t)1 << 40))
+        return QNN_ERR_SHAPE;
+    qnn_status st = device_info(nullptr);
+    if (st != QNN_OK)
+        return st;
+    return launch_relu_s8((const uint8_t *)x_dev, (uint8_t *)y_dev, count, (hipStream_t)stream) ==
+                   hipSuccess
+               ? QNN_OK
+               : QNN_ERR_LAUNCH;
+}
+
+qnn_status qnn_pack_host(const uint8_t *codes, size_t count, int32_t bits, uint8_t *out)
+{
+    if (!valid_bits(bits))
+        return QNN_ERR_BITS;
+    if (count == 0)
+        return QNN_OK;
+    if (!codes || !out)
+        return QNN_ERR_NULL;
+    const unsigned mask = (1u << bits) - 1u;
+    for (size_t i = 0; i < count; ++i)
+        if (codes[i] > mask)
+            return QNN_ERR_PARAM;
+    const size_t nbytes = (count * (size_t)bits + 7) / 8;
+    memset(out, 0, nbytes);
+    const int per = 8 / bits;
+    for (size_t i = 0; i < count; ++i)
+        out[i / per] |= (uint8_t)(codes[i] << ((i % per) * bits));
+    return QNN_OK;
+}
+
+qnn_status qnn_unpack_host(const uint8_t *packed, size_t count, int32_t bits, int32_t is_signed,
+                           int32_t *out)
+{
+    if (!valid_bits(bits))
+        return QNN_ERR_BITS;
+    if (count == 0)
+        return QNN_OK;
+    if (!packed || !out)
+        return QNN_ERR_NULL;
+    const int per = 8 / bits;
+    const unsigned mask = (1u << bits) - 1u;
+    for (size_t i = 0; i < count; ++i) {
+        const unsigned code = (packed[i / per] >> ((i % per) * bits)) & mask;
+        int32_t v;
+        if (bits == 1)
+            v = code ? 1 : -1;
+        else if (is_signed && (code >> (bits - 1)))
+            v = (int32_t)code - (1 << bits);
+        else
+            v = (int32_t)code;
+        out[i] = v;
+    }
+    return QNN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,95 @@
+// Internal declarations shared by the host dispatcher and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace qnn {
+
+// Division by a run-time constant: q = (umulhi(n, mul) + n) >> shr, exact for
+// 0 <= n < 2^31 (round-up magic number; d = 1 gives mul = 1, shr = 0).
+struct FastDiv {
+    uint32_t d, mul, shr;
+};
+
+inline FastDiv make_fastdiv(uint32_t d)
+{
+    FastDiv f;
+    f.d = d;
+    uint32_t l = 0;
+    while ((1ull << l) < d)
+        ++l;
+    f.shr = l;
+    f.mul = (uint32_t)((((1ull << l) - d) << 32) / d + 1);
+    return f;
+}
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f)
+{
+    return (__umulhi(n, f.mul) + n) >> f.shr;
+}
+
+enum { EPI_REQUANT = 0, EPI_THRESH1 = 1, EPI_RAW32 = 2 };
+
+// Arguments of the int8-MFMA implicit-GEMM convolution (8/4/2-bit inputs).
+// GEMM view: rows = output channels (A = weights), columns = output pixels
+// (B = im2col of the input tile held in local memory), K = kh*kw*C.
+struct ConvArgs {
+    const uint8_t *x;      // packed NHWC input
+    const uint8_t *w;      // packed OHWI weights
+    uint8_t *y;            // packed NHWC output (codes) or int32 [pix][M]
+    const int32_t *bias, *mult;
+    const int8_t *shift;
+    int32_t n, h, w_, pb;  // input size, packed bytes per pixel
+    int32_t c8;            // channels (= bytes of an unpacked int8 pixel)
+    int32_t m, kh, kw, sh, sw, ph, pw, ho, wo;
+    int32_t wrow;          // packed bytes per filter bank
+    int32_t epi, clip_lo, clip_hi, ypb;  // ypb: output bytes per pixel
+    // tiling of the output: tile = ti images x th rows x tw columns
+    int32_t ti, th, tw, tiles_x, tiles_y, ntiles;
+    int32_t hh, hwd, ps;   // halo rows / columns, local-memory pixel stride
+    int32_t kchunks, ksteps, kp;  // 16-byte K chunks, 64-deep MFMA steps, weight row stride
+    int32_t ot_b;          // output-tile bytes per pixel in local memory
+    int32_t off_tab, off_wsum, off_x, off_out, lds_bytes;
+    int32_t row_mode, row_len, cpr;  // K walk per filter row when C*1B is not a multiple of 16
+    FastDiv div_pbq;       // packed 16-byte (or 4-byte) quads per pixel
+    FastDiv div_hwd;       // halo columns
+    FastDiv div_hh;        // halo rows
+    FastDiv div_tile_px;   // th*tw
+    FastDiv div_tw;
+    FastDiv div_tx, div_ty;   // tiles_x, tiles_y
+    FastDiv div_obq;       // output quads per pixel in the copy-out
+    int32_t pbq, quad16;   // quads per pixel, 1 if the quad is 16 bytes else 4 bytes
+    int32_t ob0, obn, obq, oquad16;  // copy-out byte offset, byte count, quads, quad size flag
+};
+
+// Arguments of the INT-1 XNOR/popcount convolution.
+struct XnorArgs {
+    const uint32_t *x;     // packed NHWC bits, cd dwords per pixel
+    const uint32_t *w;     // packed M x kh x kw x C bits, kd dwords per bank
+    uint8_t *y;
+    const int32_t *bias, *thresh;
+    int32_t n, h, w_, cd;
+    int32_t m, kh, kw, sh, sw, ph, pw, ho, wo;
+    int32_t kd, kbits, epi, ypb;
+    int32_t npix;
+    FastDiv div_wo, div_ho, div_cd, div_kw;
+};
+
+struct PoolArgs {
+    const uint8_t *x;
+    uint8_t *y;
+    int32_t n, h, w_, pbd;     // pbd: dwords per pixel
+    int32_t kh, kw, sh, sw, ho, wo;
+    int32_t total;             // output dwords
+    FastDiv div_pbd, div_wo, div_ho;
+};
+
+hipError_t launch_conv_mfma_b8(const ConvArgs &a, int mr, int nc, int al16, dim3 grid, hipStream_t s);
+hipError_t launch_conv_mfma_b4(const ConvArgs &a, int mr, int nc, int al16, dim3 grid, hipStream_t s);
+hipError_t launch_conv_mfma_b2(const ConvArgs &a, int mr, int nc, int al16, dim3 grid, hipStream_t s);
+hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s);
+hipError_t launch_maxpool(const PoolArgs &a, int bits, hipStream_t s);
+hipError_t launch_relu_s8(const uint8_t *x, uint8_t *y, size_t count, hipStream_t s);
+
+}  // namespace qnn

@@ -1,0 +1,168 @@
+"""C-ABI checks that need no GPU: the library loads, exports every function
+its header declares, validates arguments on the host (before any device
+call) and its host packing helpers agree with the generator and the oracle."""
+import ctypes
+
+import numpy as np
+import pytest
+
+import synth
+
+
+@pytest.fixture(scope="module")
+def q():
+    import paper_1908_11263_amd as q
+    return q
+
+
+@pytest.fixture(scope="module")
+def L(q):
+    return q.lib()
+
+
+def test_exports_every_header_function(q, L):
+    names = q.qnn.header_functions()
+    assert len(names) >= 12
+    for name in names:
+        assert hasattr(L, name), name
+    assert L.qnn_abi_version() == 1
+
+
+def test_status_strings(q, L):
+    for code in range(10):
+        assert L.qnn_status_string(code)
+    assert L.qnn_status_string(123) == b"unknown status"
+
+
+def test_pixel_and_tensor_bytes(q, L):
+    T = q.qnn.Tensor
+    assert L.qnn_pixel_bytes(ctypes.byref(T(1, 1, 1, 64, 4))) == 32
+    assert L.qnn_pixel_bytes(ctypes.byref(T(1, 1, 1, 3, 8))) == 3
+    assert L.qnn_pixel_bytes(ctypes.byref(T(1, 1, 1, 5, 2))) == 2
+    assert L.qnn_pixel_bytes(ctypes.byref(T(1, 1, 1, 10, 32))) == 40
+    assert L.qnn_tensor_bytes(ctypes.byref(T(64, 32, 32, 64, 4))) == 64 * 32 * 32 * 32
+    assert L.qnn_tensor_bytes(None) == 0
+
+
+def test_out_shape(q):
+    assert q.out_shape((1, 16, 16, 32), 8, 32, 3, 3, (1, 1), (1, 1)) == (1, 16, 16, 32, 8)
+    assert q.out_shape((2, 9, 7, 256), 1, 70, 3, 3, (2, 2), (1, 1), "thresh1") == (2, 5, 4, 70, 1)
+    assert q.out_shape((4, 4, 4, 64), 8, 10, 4, 4, (1, 1), (0, 0), "raw32") == (4, 1, 1, 10, 32)
+    with pytest.raises(q.QnnError) as e:
+        q.out_shape((1, 2, 2, 32), 8, 4, 5, 5, (1, 1), (0, 0))
+    assert e.value.status == 3
+
+
+FAKE = 1 << 20  # a 16-byte aligned non-NULL address; never dereferenced
+
+
+def call_conv(q, L, xs, bits, m, g, epi, ys, xp=FAKE, wp=FAKE, yp=FAKE):
+    T, G, E = q.qnn.Tensor, q.qnn.ConvGeom, q.qnn.Epi
+    return L.qnn_conv2d(ctypes.byref(T(*xs, bits)), xp, m, wp, ctypes.byref(G(*g)),
+                        ctypes.byref(E(*epi)), ctypes.byref(T(*ys)), yp, None)
+
+
+REQ8 = (0, None, FAKE, FAKE, None, 0, 255)
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(bits=3), 2),                                    # bits not in {1,2,4,8}
+    (dict(xs=(1, 0, 4, 32)), 3),                          # empty image
+    (dict(m=0), 3),                                       # no filters
+    (dict(g=(0, 3, 1, 1, 1, 1)), 4),                      # kernel 0
+    (dict(g=(3, 3, 0, 1, 1, 1)), 4),                      # stride 0
+    (dict(g=(3, 3, 1, 1, -1, 1)), 4),                     # negative pad
+    (dict(g=(9, 9, 1, 1, 0, 0), ys=(1, 0, 0, 32, 8)), 3),  # kernel larger than padded input
+    (dict(ys=(1, 4, 4, 32, 4)), 2),                       # wrong output bit-width
+    (dict(ys=(1, 4, 5, 32, 8)), 3),                       # wrong output shape
+    (dict(epi=(0, None, None, FAKE, None, 0, 255)), 1),   # REQUANT without multipliers
+    (dict(epi=(0, None, FAKE, FAKE, None, 0, 256)), 4),   # clip above 2^bits - 1
+    (dict(epi=(0, None, FAKE, FAKE, None, 5, 4)), 4),     # clip_lo > clip_hi
+    (dict(epi=(0, None, FAKE, FAKE, None, -1, 4)), 4),    # negative clip_lo
+    (dict(epi=(1, None, None, None, FAKE, 0, 0)), 2),     # THRESH1 on 8-bit data
+    (dict(epi=(7, None, None, None, None, 0, 0)), 4),     # unknown epilogue
+    (dict(xs=(1, 4, 4, 3), ys=(1, 4, 4, 32, 8)), 5),      # 3-byte pixels
+    (dict(xp=FAKE + 4), 5),                               # misaligned input pointer
+    (dict(yp=FAKE + 8), 5),                               # misaligned output pointer
+    (dict(xp=None), 1),                                   # NULL input
+    (dict(wp=None), 1),                                   # NULL weights
+    (dict(xs=(1, 4, 4, 8192), g=(3, 3, 1, 1, 1, 1)), 6),  # K = 73728 > INT-8 limit
+])
+def test_conv_validation_on_host(q, L, case, status):
+    args = dict(xs=(1, 4, 4, 32), bits=8, m=32, g=(3, 3, 1, 1, 1, 1), epi=REQ8,
+                ys=(1, 4, 4, 32, 8))
+    args.update(case)
+    assert call_conv(q, L, **args) == status
+
+
+def test_int1_requires_threshold_or_raw(q, L):
+    assert call_conv(q, L, (1, 4, 4, 32), 1, 8, (3, 3, 1, 1, 1, 1), (0, None, FAKE, FAKE, None, 0, 1),
+                     (1, 4, 4, 8, 1)) == 2
+    assert call_conv(q, L, (1, 4, 4, 32), 1, 8, (3, 3, 1, 1, 1, 1), (1, None, None, None, None, 0, 0),
+                     (1, 4, 4, 8, 1)) == 1
+
+
+def test_unsupported_local_memory(q, L):
+    """A filter bank too long for one local-memory tile is refused on the host."""
+    st = call_conv(q, L, (1, 8, 8, 4096), 8, 16, (3, 3, 1, 1, 1, 1), REQ8, (1, 8, 8, 16, 8))
+    assert st == 7
+
+
+def test_batch_zero_is_ok_without_pointers(q, L):
+    assert call_conv(q, L, (0, 4, 4, 32), 8, 32, (3, 3, 1, 1, 1, 1), REQ8, (0, 4, 4, 32, 8),
+                     xp=None, wp=None, yp=None) == 0
+
+
+def test_valid_call_without_gpu_reports_device(q, L):
+    import torch
+    if torch.cuda.is_available():
+        pytest.skip("a GPU is present")
+    assert call_conv(q, L, (1, 4, 4, 32), 8, 32, (3, 3, 1, 1, 1, 1), REQ8, (1, 4, 4, 32, 8)) == 8
+    assert L.qnn_device_check() == 8
+
+
+def test_pool_and_relu_validation(q, L):
+    T = q.qnn.Tensor
+    x = T(1, 4, 4, 32, 8)
+    assert L.qnn_maxpool2d(ctypes.byref(T(1, 4, 4, 32, 1)), FAKE, 2, 2, 2, 2,
+                           ctypes.byref(T(1, 2, 2, 32, 1)), FAKE, None) == 2
+    assert L.qnn_maxpool2d(ctypes.byref(x), FAKE, 0, 2, 2, 2, ctypes.byref(T(1, 2, 2, 32, 8)),
+                           FAKE, None) == 4
+    assert L.qnn_maxpool2d(ctypes.byref(x), FAKE, 2, 2, 2, 2, ctypes.byref(T(1, 3, 2, 32, 8)),
+                           FAKE, None) == 3
+    assert L.qnn_maxpool2d(ctypes.byref(x), FAKE, 5, 5, 1, 1, ctypes.byref(T(1, 0, 0, 32, 8)),
+                           FAKE, None) == 3
+    assert L.qnn_relu_s8(FAKE, FAKE, 0, None) == 0
+    assert L.qnn_relu_s8(None, FAKE, 4, None) == 1
+    assert L.qnn_relu_s8(FAKE + 1, FAKE, 4, None) == 5
+
+
+def test_linear_validation(q, L):
+    T, E = q.qnn.Tensor, q.qnn.Epi
+    x = T(4, 4, 4, 64, 8)
+    e = E(2, None, None, None, None, 0, 0)
+    assert L.qnn_linear(ctypes.byref(x), FAKE, 10, FAKE, ctypes.byref(e),
+                        ctypes.byref(T(4, 1, 2, 10, 32)), FAKE, None) == 3
+    assert L.qnn_linear(ctypes.byref(x), FAKE, 10, FAKE, ctypes.byref(e),
+                        ctypes.byref(T(4, 1, 1, 10, 8)), FAKE, None) == 2
+
+
+@pytest.mark.parametrize("bits", [1, 2, 4, 8])
+def test_host_pack_unpack_agree_with_generator_and_oracle(q, orc, bits):
+    rng = np.random.default_rng(bits)
+    for count in (1, 5, 8, 33, 1000):
+        codes = rng.integers(0, 1 << bits, size=count)
+        packed = q.pack_host(codes.astype(np.uint8), bits)
+        assert np.array_equal(packed, synth.pack_codes(codes[None, :], bits)[0])
+        for signed in (False, True):
+            assert np.array_equal(q.unpack_host(packed, count, bits, signed),
+                                  orc.unpack(packed, count, bits, signed))
+
+
+def test_host_pack_rejects_out_of_range(q, L):
+    codes = np.array([0, 16], dtype=np.uint8)
+    out = np.zeros(1, dtype=np.uint8)
+    assert L.qnn_pack_host(codes.ctypes.data_as(ctypes.c_void_p), 2, 4,
+                           out.ctypes.data_as(ctypes.c_void_p)) == 4
+    assert L.qnn_pack_host(codes.ctypes.data_as(ctypes.c_void_p), 2, 3,
+                           out.ctypes.data_as(ctypes.c_void_p)) == 2
