@@ -100,6 +100,174 @@ __device__ __forceinline__ int64_t round_shift(int64_t t, int s)
     return s == 0 ? t : (t >> s) + ((t >> (s - 1)) & 1);
 }
 
+// Stage 16 packed weight bytes (natural order) as int8 at dst: 16, 32 or 64
+// bytes for 8, 4, 2 bits (4-/2-bit codes scaled by 16 / 64).
+template <int BITS>
+__device__ __forceinline__ void stage_w16(int8_t *dst, uint4 v)
+{
+    if (BITS == 8) {
+        *(uint4 *)dst = v;
+    } else if (BITS == 4) {
+        uint4 o0, o1;
+        o0.x = w4_to_s8x16(v.x & 0xFFFFu);
+        o0.y = w4_to_s8x16(v.x >> 16);
+        o0.z = w4_to_s8x16(v.y & 0xFFFFu);
+        o0.w = w4_to_s8x16(v.y >> 16);
+        o1.x = w4_to_s8x16(v.z & 0xFFFFu);
+        o1.y = w4_to_s8x16(v.z >> 16);
+        o1.z = w4_to_s8x16(v.w & 0xFFFFu);
+        o1.w = w4_to_s8x16(v.w >> 16);
+        *(uint4 *)dst = o0;
+        *(uint4 *)(dst + 16) = o1;
+    } else {
+        const uint32_t d[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            uint4 o;
+            o.x = w2_to_s8x64(d[i] & 0xFFu);
+            o.y = w2_to_s8x64((d[i] >> 8) & 0xFFu);
+            o.z = w2_to_s8x64((d[i] >> 16) & 0xFFu);
+            o.w = w2_to_s8x64(d[i] >> 24);
+            *(uint4 *)(dst + 16 * i) = o;
+        }
+    }
+}
+
+// Per-channel requantization plan.  For mult > 0 the compressed code is a
+// non-decreasing step function of the accumulator: it is lo up to a_base and
+// hi from a_base + D on, and in between
+//   y = Q + ((d * mult + R) >> shift),  d = acc - a_base in [0, D],
+// with (a_base + bias) * mult + 2^(shift-1) = Q * 2^shift + R.  When D and
+// mult fit 24 bits this is exact with one 24-bit multiply-add per output if
+// R + D * mult < 2^32 (mode 1), else with a 32x32->64 multiply-add (mode 2);
+// other channels use the direct 64-bit form.  Two 16-byte words per channel:
+//   modes 1, 2: e0 = {a_base, D, mult, R}, e1 = {Q, shift, mode, 0}
+//   direct:     e0 = {bias lo, bias hi, mult, shift}, e1 = {0, 0, 0, 0}
+// (RAW32 uses the slow word's bias only.)
+// floor(a / b) for b > 0 and |a| < 2^52: the double quotient is within one
+// of the true one and is corrected exactly in integers.
+__device__ __forceinline__ int64_t floor_div_pos(int64_t a, int64_t b)
+{
+    int64_t q = (int64_t)floor((double)a / (double)b);
+    const int64_t r = a - q * b;
+    if (r < 0)
+        q -= 1;
+    else if (r >= b)
+        q += 1;
+    return q;
+}
+
+__device__ __forceinline__ void requant_plan(int64_t bias, int32_t mult, int32_t shift, int32_t lo,
+                                             int32_t hi, bool requant, int4 &e0, int4 &e1)
+{
+    e0 = make_int4((int32_t)(uint32_t)(uint64_t)bias, (int32_t)(bias >> 32), mult, shift);
+    e1 = make_int4(0, 0, 0, 0);
+    if (!requant || mult <= 0 || shift > 30 || bias > ((int64_t)1 << 40) || bias < -((int64_t)1 << 40))
+        return;
+    const int64_t half = shift > 0 ? ((int64_t)1 << (shift - 1)) : 0;
+    const int64_t two_s = (int64_t)1 << shift;
+    // smallest accumulator whose code reaches p: ceil((p 2^s - half) / mult) - bias
+    const int64_t t_lo = -floor_div_pos(half - (int64_t)lo * two_s, mult) - bias;
+    const int64_t t_hi = -floor_div_pos(half - (int64_t)hi * two_s, mult) - bias;
+    const int64_t a_base = t_lo - 1;
+    const int64_t D = t_hi - a_base;
+    if (a_base < INT32_MIN || t_hi > INT32_MAX || D < 0 || D >= (1 << 24) || mult >= (1 << 24))
+        return;
+    const int64_t n0 = (a_base + bias) * (int64_t)mult + half;
+    const int64_t Q = n0 >> shift;
+    const int64_t R = n0 - Q * two_s;
+    if (Q < INT32_MIN || Q > INT32_MAX)
+        return;
+    e0 = make_int4((int32_t)a_base, (int32_t)D, mult, (int32_t)(uint32_t)R);
+    // mode 1: R + D * mult fits 32 bits; mode 2: it needs the 64-bit product
+    e1 = make_int4((int32_t)Q, shift, R + D * (int64_t)mult < ((int64_t)1 << 32) ? 1 : 2, 0);
+}
+
+// One batch of U packed-input quads of a tile: issue the loads ...
+template <int BITS, bool Q16, int U>
+__device__ __forceinline__ void halo_issue(const ConvArgs &a, int b0, int totq, int n0, int iy0,
+                                           int ix0, uint4 *v, int *dst)
+{
+    constexpr int QB = Q16 ? 16 : 4;
+    constexpr int QU = QB * 8 / BITS;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        const int idx = b0 + u * 256;
+        v[u] = make_uint4(0, 0, 0, 0);
+        dst[u] = -1;
+        if (idx < totq) {
+            const int pix = (int)fdiv((uint32_t)idx, a.div_pbq);
+            const int q = idx - pix * a.pbq;
+            const int hrow = (int)fdiv((uint32_t)pix, a.div_hwd);
+            const int hx = pix - hrow * a.hwd;
+            const int tI = (int)fdiv((uint32_t)hrow, a.div_hh);
+            const int hy = hrow - tI * a.hh;
+            const int nn = n0 + tI, iy = iy0 + hy, ix = ix0 + hx;
+            dst[u] = pix * a.ps + q * QU;
+            if (nn < a.n && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w_) {
+                const uint8_t *src = a.x + (((size_t)nn * a.h + iy) * a.w_ + ix) * a.pb + q * QB;
+                if (Q16)
+                    v[u] = *(const uint4 *)src;
+                else
+                    v[u].x = *(const uint32_t *)src;
+            }
+        }
+    }
+}
+
+// ... and unpack them into the LDS tile.
+template <int BITS, bool Q16, int U>
+__device__ __forceinline__ void halo_store(uint8_t *sX, const uint4 *v, const int *dst)
+{
+    constexpr int W = 32 / BITS;  // unpacked bytes per packed word
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        if (dst[u] >= 0) {
+            uint8_t *d = sX + dst[u];
+            stage_word<BITS>(d, v[u].x);
+            if (Q16) {
+                stage_word<BITS>(d + W, v[u].y);
+                stage_word<BITS>(d + 2 * W, v[u].z);
+                stage_word<BITS>(d + 3 * W, v[u].w);
+            }
+        }
+    }
+}
+
+// Whole tile (or the part after the first batch) in batches of U.
+template <int BITS, bool Q16, int U>
+__device__ __forceinline__ void halo_stage_from(const ConvArgs &a, uint8_t *sX, int b_first, int n0,
+                                                int iy0, int ix0)
+{
+    const int totq = a.ti * a.hh * a.hwd * a.pbq;
+    for (int b0 = b_first; b0 < totq; b0 += 256 * U) {
+        uint4 v[U];
+        int dst[U];
+        halo_issue<BITS, Q16, U>(a, b0, totq, n0, iy0, ix0, v, dst);
+        halo_store<BITS, Q16, U>(sX, v, dst);
+    }
+}
+
+// Tile index -> first image / output row / output column.
+struct TileXY {
+    int n0, oy0, ox0, iy0, ix0;
+};
+
+__device__ __forceinline__ TileXY tile_xy(const ConvArgs &a, int tile)
+{
+    TileXY r;
+    const int tq = (int)fdiv((uint32_t)tile, a.div_tx);
+    const int tx = tile - tq * a.tiles_x;
+    const int tn = (int)fdiv((uint32_t)tq, a.div_ty);
+    const int ty = tq - tn * a.tiles_y;
+    r.n0 = tn * a.ti;
+    r.oy0 = ty * a.th;
+    r.ox0 = tx * a.tw;
+    r.iy0 = r.oy0 * a.sh - a.ph;
+    r.ix0 = r.ox0 * a.sw - a.pw;
+    return r;
+}
+
 template <int BITS, int MR, int NC, bool AL16>
 __global__ void __launch_bounds__(256) conv_mfma_kernel(ConvArgs a)
 {
@@ -115,14 +283,54 @@ __global__ void __launch_bounds__(256) conv_mfma_kernel(ConvArgs a)
     int32_t *sTab = (int32_t *)(smem + a.off_tab);
     int32_t *sNat = sTab + kch;
     int32_t *sVld = sNat + kch;
-    int32_t *sWsum = (int32_t *)(smem + a.off_wsum);
+    int32_t *sWsum = (int32_t *)(smem + a.off_wsum);           // [MT] filter sums (8 bits), [4] votes
+    int4 *sEpi = (int4 *)(smem + a.off_wsum + 4 * MT + 16);      // [MT][2] requantization plans
     uint8_t *sX = smem + a.off_x;
     uint8_t *sOut = smem + a.off_out;
 
-    // (1) K-chunk tables: chunk j = 16 consecutive K bytes.  sTab: offset of
-    // the chunk in the input tile relative to a pixel's top-left tap; sNat:
-    // offset in the natural (ky, kx, c) order of a filter bank; sVld: bytes of
-    // the chunk that belong to the filter (the rest meets zero weights).
+    // ---- prologue: every independent load is issued before any is used ----
+    // per-channel epilogue parameters (one thread per channel)
+    int32_t p_bias = 0, p_mult = 0, p_shift = 0;
+    if (tid < MT && m0 + tid < a.m) {
+        if (a.bias)
+            p_bias = a.bias[m0 + tid];
+        if (a.epi == EPI_REQUANT) {
+            p_mult = a.mult[m0 + tid];
+            p_shift = a.shift[m0 + tid];
+        }
+    }
+    // filter tile, first batch (contiguous rows, natural order = chunk order)
+    const bool wfast = !a.row_mode && (a.wrow & 15) == 0;
+    const int qrow = a.wrow >> 4;
+    const int nq = MT * qrow;
+    constexpr int UW = 8;
+    uint4 wq[UW];
+    if (wfast) {
+#pragma unroll
+        for (int u = 0; u < UW; ++u) {
+            const int idx = tid + u * 256;
+            const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
+            wq[u] = make_uint4(0, 0, 0, 0);
+            if (idx < nq && m0 + row < a.m)
+                wq[u] = *(const uint4 *)(a.w + (size_t)(m0 + row) * a.wrow + (idx - row * qrow) * 16);
+        }
+    }
+    // input tile of the first pixel tile, first batch
+    int tile = blockIdx.x;
+    TileXY T = tile_xy(a, tile < a.ntiles ? tile : 0);
+    constexpr int UH = 4;
+    uint4 hq[UH];
+    int hd[UH];
+    const int totq = a.ti * a.hh * a.hwd * a.pbq;
+    if (a.quad16)
+        halo_issue<BITS, true, UH>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
+    else
+        halo_issue<BITS, false, UH>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
+
+    // K-chunk tables: chunk j = 16 consecutive K bytes.  sTab: offset of the
+    // chunk in the input tile relative to a pixel's top-left tap; sNat: offset
+    // in the natural (ky, kx, c) order of a filter bank; sVld: bytes of the
+    // chunk that belong to the filter (the rest meets zero weights).
     for (int j = tid; j < kch; j += 256) {
         int hoff = 0, nat = 0, vld = 0;
         if (j < a.kchunks) {
@@ -146,27 +354,95 @@ __global__ void __launch_bounds__(256) conv_mfma_kernel(ConvArgs a)
     }
     __syncthreads();
 
-    // (2) Filter tile -> int8 in chunk order (rows = output channels).
+    // filter tile -> int8 (4-/2-bit codes scaled by 16 / 64), chunk order
     const int ncol = kch * 4;
-    for (int row = wv; row < MT; row += 4) {
-        const int mg = m0 + row;
-        const uint8_t *wr = a.w + (size_t)min(mg, a.m - 1) * a.wrow;
-        for (int col = lane; col < ncol; col += 64) {
-            const int j = col >> 2, d = col & 3;
-            uint32_t val = 0;
-            if (mg < a.m && 4 * d < sVld[j]) {
-                const int e = sNat[j] + 4 * d;
-                if (BITS == 8)
-                    val = *(const uint32_t *)(wr + e);
-                else if (BITS == 4)
-                    val = w4_to_s8x16(*(const uint16_t *)(wr + (e >> 1)));
-                else
-                    val = w2_to_s8x64(wr[e >> 2]);
+    if (wfast) {
+#pragma unroll
+        for (int u = 0; u < UW; ++u) {
+            const int idx = tid + u * 256;
+            if (idx < nq) {
+                const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
+                stage_w16<BITS>(sW + row * a.kp + (idx - row * qrow) * (128 / BITS), wq[u]);
             }
-            *(uint32_t *)(sW + row * a.kp + col * 4) = val;
+        }
+        for (int b0 = tid + 256 * UW; b0 < nq; b0 += 256 * UW) {
+#pragma unroll
+            for (int u = 0; u < UW; ++u) {
+                const int idx = b0 + u * 256;
+                const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
+                wq[u] = make_uint4(0, 0, 0, 0);
+                if (idx < nq && m0 + row < a.m)
+                    wq[u] = *(const uint4 *)(a.w + (size_t)(m0 + row) * a.wrow + (idx - row * qrow) * 16);
+            }
+#pragma unroll
+            for (int u = 0; u < UW; ++u) {
+                const int idx = b0 + u * 256;
+                if (idx < nq) {
+                    const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
+                    stage_w16<BITS>(sW + row * a.kp + (idx - row * qrow) * (128 / BITS), wq[u]);
+                }
+            }
+        }
+        // zero the chunks that round K up to whole MFMA steps
+        const int padc = kch - a.kchunks;
+        for (int i = tid; i < MT * padc; i += 256) {
+            const int row = i / padc;
+            *(uint4 *)(sW + row * a.kp + (a.kchunks + i - row * padc) * 16) = make_uint4(0, 0, 0, 0);
+        }
+    } else {
+        // general order (row walk for small C): one 4-byte LDS word per item
+        const int nit = MT * ncol;
+        constexpr int U = 4;
+        for (int b0 = tid; b0 < nit; b0 += 256 * U) {
+            uint32_t v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int idx = b0 + u * 256;
+                const int row = (int)fdiv((uint32_t)idx, a.div_ncol);
+                const int col = idx - row * ncol;
+                const int j = col >> 2, d = col & 3;
+                const int mg = m0 + row;
+                v[u] = 0;
+                if (idx < nit && mg < a.m && 4 * d < sVld[j]) {
+                    const uint8_t *wr = a.w + (size_t)mg * a.wrow;
+                    const int e = sNat[j] + 4 * d;
+                    if (BITS == 8)
+                        v[u] = *(const uint32_t *)(wr + e);
+                    else if (BITS == 4)
+                        v[u] = *(const uint16_t *)(wr + (e >> 1));
+                    else
+                        v[u] = wr[e >> 2];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int idx = b0 + u * 256;
+                if (idx < nit) {
+                    const int row = (int)fdiv((uint32_t)idx, a.div_ncol);
+                    const int col = idx - row * ncol;
+                    uint32_t val = v[u];
+                    if (BITS == 4)
+                        val = w4_to_s8x16(val);
+                    else if (BITS == 2)
+                        val = w2_to_s8x64(val);
+                    *(uint32_t *)(sW + row * a.kp + col * 4) = val;
+                }
+            }
+        }
+    }
+    // input tile of the first pixel tile: first batch, then the rest
+    if (tile < a.ntiles) {
+        if (a.quad16) {
+            halo_store<BITS, true, UH>(sX, hq, hd);
+            halo_stage_from<BITS, true, UH>(a, sX, tid + 256 * UH, T.n0, T.iy0, T.ix0);
+        } else {
+            halo_store<BITS, false, UH>(sX, hq, hd);
+            halo_stage_from<BITS, false, UH>(a, sX, tid + 256 * UH, T.n0, T.iy0, T.ix0);
         }
     }
     __syncthreads();
+
+    // filter sums for the unsigned 8-bit fold, then the requantization plans
     if (BITS == 8) {
         for (int row = wv; row < MT; row += 4) {
             int s = 0;
@@ -179,50 +455,50 @@ __global__ void __launch_bounds__(256) conv_mfma_kernel(ConvArgs a)
             if (lane == 0)
                 sWsum[row] = s;
         }
+        __syncthreads();
     }
+    int mode = 1;
+    if (tid < MT) {
+        int64_t b = p_bias;
+        if (BITS == 8)
+            b += 128 * (int64_t)sWsum[tid];
+        p_shift = p_shift < 0 ? 0 : (p_shift > 62 ? 62 : p_shift);
+        int4 e0, e1;
+        requant_plan(b, p_mult, p_shift, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, e0, e1);
+        if (m0 + tid >= a.m)
+            e1.z = 1;  // missing channels: code forced to 0 below
+        sEpi[2 * tid] = e0;
+        sEpi[2 * tid + 1] = e1;
+        mode = e1.z;
+    }
+    // workgroup-uniform epilogue selection: per-wave votes in LDS, then the
+    // barrier that also publishes sEpi
+    {
+        const bool v32 = __all(mode == 1);
+        const bool v64 = __all(mode == 1 || mode == 2);
+        if (lane == 0)
+            sWsum[MT + wv] = (v32 ? 1 : 0) | (v64 ? 2 : 0);
+    }
+    __syncthreads();
+    const int votes = sWsum[MT] & sWsum[MT + 1] & sWsum[MT + 2] & sWsum[MT + 3];
+    const bool all32 = (votes & 1) != 0;
+    const bool all64 = (votes & 2) != 0;
+    const bool full = m0 + MT <= a.m;
 
     const int tile_px = a.ti * a.th * a.tw;
     const int g = lane >> 4, r16 = lane & 15;
-    const int quad_b = a.quad16 ? 16 : 4;
-    const int quad_u = quad_b * 8 / BITS;  // unpacked bytes per quad
 
-    for (int tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
-        const int tq = (int)fdiv((uint32_t)tile, a.div_tx);
-        const int tx = tile - tq * a.tiles_x;
-        const int tn = (int)fdiv((uint32_t)tq, a.div_ty);
-        const int ty = tq - tn * a.tiles_y;
-        const int n0 = tn * a.ti, oy0 = ty * a.th, ox0 = tx * a.tw;
-        const int iy0 = oy0 * a.sh - a.ph, ix0 = ox0 * a.sw - a.pw;
-
-        // (3) Input tile + halo -> LDS, unpacked to int8, one quad per thread step.
-        const int totq = a.ti * a.hh * a.hwd * a.pbq;
-        for (int idx = tid; idx < totq; idx += 256) {
-            const int pix = (int)fdiv((uint32_t)idx, a.div_pbq);
-            const int q = idx - pix * a.pbq;
-            const int hrow = (int)fdiv((uint32_t)pix, a.div_hwd);
-            const int hx = pix - hrow * a.hwd;
-            const int tI = (int)fdiv((uint32_t)hrow, a.div_hh);
-            const int hy = hrow - tI * a.hh;
-            const int nn = n0 + tI, iy = iy0 + hy, ix = ix0 + hx;
-            const bool in = nn < a.n && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w_;
-            const uint8_t *src = a.x + (((size_t)(in ? nn : 0) * a.h + (in ? iy : 0)) * a.w_ +
-                                        (in ? ix : 0)) * a.pb + q * quad_b;
-            uint8_t *dst = sX + pix * a.ps + q * quad_u;
-            if (a.quad16) {
-                uint4 v = in ? *(const uint4 *)src : make_uint4(0, 0, 0, 0);
-                constexpr int U = 32 / BITS;  // unpacked bytes per packed word
-                stage_word<BITS>(dst, v.x);
-                stage_word<BITS>(dst + U, v.y);
-                stage_word<BITS>(dst + 2 * U, v.z);
-                stage_word<BITS>(dst + 3 * U, v.w);
-            } else {
-                uint32_t v = in ? *(const uint32_t *)src : 0u;
-                stage_word<BITS>(dst, v);
-            }
+    for (bool first = true; tile < a.ntiles; tile += gridDim.x, first = false) {
+        if (!first) {
+            T = tile_xy(a, tile);
+            if (a.quad16)
+                halo_stage_from<BITS, true, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
+            else
+                halo_stage_from<BITS, false, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
+            __syncthreads();
         }
-        __syncthreads();
 
-        // (4) Main loop: MR x NC MFMA tiles per 64-deep K step.
+        // ---- main loop: MR x NC MFMA tiles per 64-deep K step ----
         int base[NC];
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
@@ -243,87 +519,179 @@ __global__ void __launch_bounds__(256) conv_mfma_kernel(ConvArgs a)
             for (int c = 0; c < NC; ++c)
                 acc[t][c] = (v4i){0, 0, 0, 0};
         const int8_t *aRow = sW + r16 * a.kp + g * 16;
-#pragma unroll 2
-        for (int ks = 0; ks < a.ksteps; ++ks) {
+        // software pipeline: fragments of K step ks + 1 are read while the
+        // MFMAs of step ks run
+        v4i av[MR], bv[NC];
+        auto load_frags = [&](int ks, v4i *A, v4i *B) {
             const int off = sTab[ks * 4 + g];
-            v4i av[MR], bv[NC];
 #pragma unroll
             for (int t = 0; t < MR; ++t)
-                av[t] = *(const v4i *)(aRow + t * 16 * a.kp + ks * 64);
+                A[t] = *(const v4i *)(aRow + t * 16 * a.kp + ks * 64);
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
                 const uint8_t *bp = sX + base[c] + off;
                 if (AL16) {
-                    bv[c] = *(const v4i *)bp;
+                    B[c] = *(const v4i *)bp;
                 } else {
                     const int32_t *b4 = (const int32_t *)bp;
-                    bv[c] = (v4i){b4[0], b4[1], b4[2], b4[3]};
+                    B[c] = (v4i){b4[0], b4[1], b4[2], b4[3]};
                 }
             }
+        };
+        load_frags(0, av, bv);
+        for (int ks = 0; ks < a.ksteps; ++ks) {
+            v4i an[MR], bn[NC];
+            if (ks + 1 < a.ksteps)
+                load_frags(ks + 1, an, bn);
 #pragma unroll
             for (int t = 0; t < MR; ++t)
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
                     acc[t][c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(av[t], bv[c], acc[t][c], 0, 0, 0);
+#pragma unroll
+            for (int t = 0; t < MR; ++t)
+                av[t] = an[t];
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                bv[c] = bn[c];
         }
 
-        // (5) Epilogue.  Lane (r16, g) of tile (t, c) holds channels
-        // t*16 + 4g + {0..3} of pixel c*16 + r16 of its wave.
+        // ---- epilogue: lane (r16, g) of tile (t, c) holds channels
+        // t*16 + 4g + {0..3} of pixel c*16 + r16 of its wave ----
+        int gpix[NC];
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             const int p = wv * 16 * NC + c * 16 + r16;
-            int gpix = -1;
+            gpix[c] = -1;
             if (p < tile_px) {
                 const int tI = (int)fdiv((uint32_t)p, a.div_tile_px);
                 const int rem = p - tI * a.th * a.tw;
                 const int py = (int)fdiv((uint32_t)rem, a.div_tw);
                 const int px = rem - py * a.tw;
-                const int nn = n0 + tI, oy = oy0 + py, ox = ox0 + px;
+                const int nn = T.n0 + tI, oy = T.oy0 + py, ox = T.ox0 + px;
                 if (nn < a.n && oy < a.ho && ox < a.wo)
-                    gpix = (nn * a.ho + oy) * a.wo + ox;
+                    gpix[c] = (nn * a.ho + oy) * a.wo + ox;
             }
+        }
+        if (a.epi == EPI_RAW32) {
 #pragma unroll
-            for (int t = 0; t < MR; ++t) {
-                const int mb = t * 16 + 4 * g;
-                uint32_t packed = 0;
+            for (int t = 0; t < MR; ++t)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int m = m0 + mb + i;
-                    if (m >= a.m)
+                    const int mrow = t * 16 + 4 * g + i;
+                    if (m0 + mrow >= a.m)
                         continue;
-                    int64_t accv = acc[t][c][i];
-                    if (BITS == 8)
-                        accv += 128 * (int64_t)sWsum[mb + i];
-                    else if (BITS == 4)
-                        accv >>= 4;
-                    else
-                        accv >>= 6;
-                    const int64_t v = accv + (a.bias ? (int64_t)a.bias[m] : 0);
-                    if (a.epi == EPI_RAW32) {
-                        if (gpix >= 0)
-                            ((int32_t *)a.y)[(size_t)gpix * a.m + m] = (int32_t)(uint32_t)(uint64_t)v;
-                    } else {
-                        int s = a.shift[m];
-                        s = s < 0 ? 0 : (s > 62 ? 62 : s);
-                        int64_t r = round_shift(v * (int64_t)a.mult[m], s);
-                        r = r < a.clip_lo ? a.clip_lo : (r > a.clip_hi ? a.clip_hi : r);
-                        packed |= (uint32_t)r << (i * BITS);
+                    const int4 e0 = sEpi[2 * mrow];
+                    const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);
+#pragma unroll
+                    for (int c = 0; c < NC; ++c) {
+                        int32_t acc32 = acc[t][c][i];
+                        if (BITS == 4)
+                            acc32 >>= 4;
+                        else if (BITS == 2)
+                            acc32 >>= 6;
+                        if (gpix[c] >= 0)
+                            ((int32_t *)a.y)[(size_t)gpix[c] * a.m + m0 + mrow] =
+                                (int32_t)(uint32_t)(uint64_t)(acc32 + bt);
                     }
                 }
-                if (a.epi != EPI_RAW32 && p < tile_px) {
-                    uint8_t *o = sOut + p * a.ot_b + mb * BITS / 8;
-                    if (BITS == 8)
-                        *(uint32_t *)o = packed;
-                    else if (BITS == 4)
-                        *(uint16_t *)o = (uint16_t)packed;
-                    else
-                        *o = (uint8_t)packed;
+        } else {
+            uint32_t packed[MR][NC];
+#pragma unroll
+            for (int t = 0; t < MR; ++t)
+#pragma unroll
+                for (int c = 0; c < NC; ++c)
+                    packed[t][c] = 0;
+            if (all32 || all64) {
+                // plan form: code = clip(Q + ((clamp(acc - a_base, 0, D) * mult + R) >> shift))
+#pragma unroll
+                for (int t = 0; t < MR; ++t) {
+                    int4 e0[4], e1[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        e0[i] = sEpi[2 * (t * 16 + 4 * g + i)];
+                        e1[i] = sEpi[2 * (t * 16 + 4 * g + i) + 1];
+                    }
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const bool live = full || (m0 + t * 16 + 4 * g + i < a.m);
+#pragma unroll
+                        for (int c = 0; c < NC; ++c) {
+                            int32_t acc32 = acc[t][c][i];
+                            if (BITS == 4)
+                                acc32 >>= 4;
+                            else if (BITS == 2)
+                                acc32 >>= 6;
+                            const int32_t d = __builtin_elementwise_sub_sat(acc32, e0[i].x);
+                            const uint32_t dc = (uint32_t)min(max(d, 0), e0[i].y);
+                            uint32_t q;
+                            if (all32) {
+                                q = (__umul24(dc, (uint32_t)e0[i].z) + (uint32_t)e0[i].w) >> e1[i].y;
+                            } else {
+                                const uint64_t tt = (uint64_t)dc * (uint32_t)e0[i].z + (uint32_t)e0[i].w;
+                                q = (uint32_t)(tt >> e1[i].y);
+                            }
+                            int32_t code = min(max(e1[i].x + (int32_t)q, a.clip_lo), a.clip_hi);
+                            if (!live)
+                                code = 0;
+                            packed[t][c] |= (uint32_t)code << (i * BITS);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
                 }
+            } else {
+                // general form, channel by channel
+#pragma unroll
+                for (int t = 0; t < MR; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int mrow = t * 16 + 4 * g + i;
+                        if (m0 + mrow >= a.m)
+                            continue;
+                        const int4 e0 = sEpi[2 * mrow];
+                        const int4 e1 = sEpi[2 * mrow + 1];
+#pragma unroll
+                        for (int c = 0; c < NC; ++c) {
+                            int32_t acc32 = acc[t][c][i];
+                            if (BITS == 4)
+                                acc32 >>= 4;
+                            else if (BITS == 2)
+                                acc32 >>= 6;
+                            int64_t r;
+                            if (e1.z) {
+                                const int32_t d = __builtin_elementwise_sub_sat(acc32, e0.x);
+                                const uint32_t dc = (uint32_t)min(max(d, 0), e0.y);
+                                const uint64_t tt = (uint64_t)dc * (uint32_t)e0.z + (uint32_t)e0.w;
+                                r = (int64_t)e1.x + (int64_t)(tt >> e1.y);
+                            } else {
+                                const int64_t v = (int64_t)acc32 +
+                                    (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);
+                                r = round_shift(v * (int64_t)e0.z, e0.w);
+                            }
+                            r = r < a.clip_lo ? a.clip_lo : (r > a.clip_hi ? a.clip_hi : r);
+                            packed[t][c] |= (uint32_t)r << (i * BITS);
+                        }
+                    }
             }
+#pragma unroll
+            for (int t = 0; t < MR; ++t)
+#pragma unroll
+                for (int c = 0; c < NC; ++c) {
+                    const int p = wv * 16 * NC + c * 16 + r16;
+                    if (p < tile_px) {
+                        uint8_t *o = sOut + p * a.ot_b + (t * 16 + 4 * g) * BITS / 8;
+                        if (BITS == 8)
+                            *(uint32_t *)o = packed[t][c];
+                        else if (BITS == 4)
+                            *(uint16_t *)o = (uint16_t)packed[t][c];
+                        else
+                            *o = (uint8_t)packed[t][c];
+                    }
+                }
         }
         __syncthreads();
 
-        // (6) Coalesced copy of the packed output tile.
+        // ---- coalesced copy of the packed output tile ----
         if (a.epi != EPI_RAW32) {
             const int ob0 = m0 * BITS / 8;
             const int obn = min(a.ot_b, a.ypb - ob0);
@@ -335,7 +703,7 @@ __global__ void __launch_bounds__(256) conv_mfma_kernel(ConvArgs a)
                 const int rem = p - tI * a.th * a.tw;
                 const int py = (int)fdiv((uint32_t)rem, a.div_tw);
                 const int px = rem - py * a.tw;
-                const int nn = n0 + tI, oy = oy0 + py, ox = ox0 + px;
+                const int nn = T.n0 + tI, oy = T.oy0 + py, ox = T.ox0 + px;
                 if (nn >= a.n || oy >= a.ho || ox >= a.wo)
                     continue;
                 const size_t gp = (size_t)(nn * a.ho + oy) * a.wo + ox;
@@ -361,8 +729,9 @@ hipError_t launch_conv_mfma_bits(const ConvArgs &a, int mr, int nc, int al16, di
         static bool attr_set = false;                                                           \
         auto *k = conv_mfma_kernel<BITS, MR_, NC_, (AL_ != 0)>;                                 \
         if (!attr_set) {                                                                        \
-            hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,    \
-                                160 * 1024);                                                    \
+            if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,  \
+                                    a.lds_bytes > 64 * 1024 ? 160 * 1024 : 64 * 1024) != hipSuccess) \
+                (void)hipGetLastError();                                                        \
             attr_set = true;                                                                    \
         }                                                                                       \
         hipLaunchKernelGGL(k, grid, dim3(256), a.lds_bytes, s, a);                              \

@@ -12,6 +12,7 @@ namespace {
 
 constexpr int kMaxDevices = 64;
 constexpr int kLdsBytes = 160 * 1024;
+constexpr int kPlanCus = 256;  // compute units of an MI355X; the grid uses the queried count
 
 struct DeviceInfo {
     int checked = 0;  // 0 unknown, 1 ok, -1 not usable
@@ -147,27 +148,35 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
     const int obits = a.epi == EPI_REQUANT ? bits : 32;
     const int64_t tab_bytes = 3 * 4 * (int64_t)(4 * a.ksteps);
 
-    int mr_first = a.m <= 16 ? 1 : (a.m <= 32 ? 2 : 4);
-    for (mr = mr_first; mr >= 1; mr >>= 1) {
-        for (nc = 4; nc >= 1; nc >>= 1) {
-            const int MT = 16 * mr, PT = 64 * nc;
+    // Candidates in order of preference (widest channel tile, then widest
+    // pixel tile).  Take the first that fits the local memory and still gives
+    // at least two tiles per compute unit; if none does, the one with the most
+    // tiles (small layers are latency-bound and want parallelism).
+    const int mr_first = a.m <= 16 ? 1 : (a.m <= 32 ? 2 : 4);
+    ConvArgs best = a;
+    int best_mr = 0, best_nc = 0;
+    int64_t best_units = -1;
+    for (int cmr = mr_first; cmr >= 1; cmr >>= 1) {
+        for (int cnc = 4; cnc >= 1; cnc >>= 1) {
+            const int MT = 16 * cmr, PT = 64 * cnc;
+            ConvArgs c = a;
             int ti, th, tw;
-            if ((int64_t)a.ho * a.wo >= PT) {
+            if ((int64_t)c.ho * c.wo >= PT) {
                 ti = 1;
-                tw = a.wo < PT ? a.wo : PT;
+                tw = c.wo < PT ? c.wo : PT;
                 th = PT / tw;
-                if (th > a.ho)
-                    th = a.ho;
+                if (th > c.ho)
+                    th = c.ho;
             } else {
-                ti = PT / (a.ho * a.wo);
-                if (ti > a.n)
-                    ti = a.n > 0 ? a.n : 1;
-                th = a.ho;
-                tw = a.wo;
+                ti = PT / (c.ho * c.wo);
+                if (ti > c.n)
+                    ti = c.n > 0 ? c.n : 1;
+                th = c.ho;
+                tw = c.wo;
             }
-            const int hh = (th - 1) * a.sh + a.kh;
-            const int hwd = (tw - 1) * a.sw + a.kw;
-            const int64_t w_bytes = (int64_t)MT * a.kp;
+            const int hh = (th - 1) * c.sh + c.kh;
+            const int hwd = (tw - 1) * c.sw + c.kw;
+            const int64_t w_bytes = (int64_t)MT * c.kp;
             const int64_t x_bytes = (int64_t)ti * hh * hwd * ps + 64;
             const int ot_b = obits == 32 ? 0 : MT * bits / 8;
             const int64_t o_bytes = (int64_t)PT * ot_b;
@@ -175,7 +184,7 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
             const int64_t off_tab = off;
             off += tab_bytes;
             const int64_t off_wsum = off;
-            off += 4 * MT;
+            off += 4 * MT + 16 + 32 * MT;   // filter sums, votes, requantization plans
             off = (off + 15) & ~(int64_t)15;
             const int64_t off_x = off;
             off += (x_bytes + 15) & ~(int64_t)15;
@@ -183,28 +192,45 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
             off += o_bytes;
             if (off > kLdsBytes)
                 continue;
-            a.ti = ti;
-            a.th = th;
-            a.tw = tw;
-            a.hh = hh;
-            a.hwd = hwd;
-            a.ot_b = ot_b;
-            a.off_tab = (int32_t)off_tab;
-            a.off_wsum = (int32_t)off_wsum;
-            a.off_x = (int32_t)off_x;
-            a.off_out = (int32_t)off_out;
-            a.lds_bytes = (int32_t)off;
-            a.tiles_x = (a.wo + tw - 1) / tw;
-            a.tiles_y = (a.ho + th - 1) / th;
-            const int64_t tiles_n = (a.n + ti - 1) / ti;
-            const int64_t nt = tiles_n * a.tiles_y * a.tiles_x;
+            c.ti = ti;
+            c.th = th;
+            c.tw = tw;
+            c.hh = hh;
+            c.hwd = hwd;
+            c.ot_b = ot_b;
+            c.off_tab = (int32_t)off_tab;
+            c.off_wsum = (int32_t)off_wsum;
+            c.off_x = (int32_t)off_x;
+            c.off_out = (int32_t)off_out;
+            c.lds_bytes = (int32_t)off;
+            c.tiles_x = (c.wo + tw - 1) / tw;
+            c.tiles_y = (c.ho + th - 1) / th;
+            const int64_t tiles_n = (c.n + ti - 1) / ti;
+            const int64_t nt = tiles_n * c.tiles_y * c.tiles_x;
             if (nt > (int64_t)1 << 30)
-                return QNN_ERR_UNSUPPORTED;
-            a.ntiles = (int32_t)nt;
-            return QNN_OK;
+                continue;
+            c.ntiles = (int32_t)nt;
+            const int64_t units = nt * ((c.m + MT - 1) / MT);
+            if (units >= 2 * kPlanCus) {
+                a = c;
+                mr = cmr;
+                nc = cnc;
+                return QNN_OK;
+            }
+            if (units > best_units) {
+                best = c;
+                best_units = units;
+                best_mr = cmr;
+                best_nc = cnc;
+            }
         }
     }
-    return QNN_ERR_UNSUPPORTED;
+    if (best_units < 0)
+        return QNN_ERR_UNSUPPORTED;
+    a = best;
+    mr = best_mr;
+    nc = best_nc;
+    return QNN_OK;
 }
 
 qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
@@ -316,6 +342,8 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
         a.obq = 1;
     }
     a.div_obq = make_fastdiv((uint32_t)a.obq);
+    a.div_qrow = make_fastdiv((uint32_t)(a.wrow / 16 > 0 ? a.wrow / 16 : 1));
+    a.div_ncol = make_fastdiv((uint32_t)(16 * a.ksteps));
     st = device_info(&cus);
     if (st != QNN_OK)
         return st;

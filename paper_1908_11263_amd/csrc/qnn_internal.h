@@ -59,6 +59,8 @@ struct ConvArgs {
     FastDiv div_tw;
     FastDiv div_tx, div_ty;   // tiles_x, tiles_y
     FastDiv div_obq;       // output quads per pixel in the copy-out
+    FastDiv div_qrow;      // packed 16-byte quads per filter bank
+    FastDiv div_ncol;      // 4-byte words per staged filter row
     int32_t pbq, quad16;   // quads per pixel, 1 if the quad is 16 bytes else 4 bytes
     int32_t ob0, obn, obq, oquad16;  // copy-out byte offset, byte count, quads, quad size flag
 };
