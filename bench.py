@@ -45,23 +45,27 @@ def kernel_source_sha():
     return h.hexdigest()[:16]
 
 
-def recorded_traffic():
-    """HBM bytes per launch of the headline kernel from the committed PMC
-    summary, if it was taken on the current kernel sources."""
+def recorded_profile():
+    """(HBM bytes per launch, kernel name) of the headline kernel from the
+    committed PMC summary; the byte count only if the summary was taken on the
+    current kernel sources."""
     if not os.path.exists(PROFILE):
-        return None
+        return None, None
     vals = {}
+    name = None
     with open(PROFILE) as f:
         for line in f:
+            if line.startswith("# HBM traffic of "):
+                name = line[len("# HBM traffic of "):].split(" (")[0].strip()
             if ":" in line and line.startswith("@"):
                 k, v = line[1:].split(":", 1)
                 vals[k.strip()] = v.strip()
     if vals.get("kernel_source_sha") != kernel_source_sha():
-        return None
+        return None, name
     try:
-        return int(vals["traffic_bytes_per_launch"])
+        return int(vals["traffic_bytes_per_launch"]), name
     except (KeyError, ValueError):
-        return None
+        return None, name
 
 
 class ConvStep:
@@ -269,9 +273,10 @@ def main():
         return
     L = head_step.L
     achieved = 2 * head_step.macs / head_sec / 1e12
+    traffic, kname = recorded_profile()
     roofline = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_INT8_TOPS,
                 "unit": "TOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 5),
-                "traffic": recorded_traffic(), "kernel": "conv_mfma_kernel<4,4,4,true>",
+                "traffic": traffic, "kernel": kname or "conv_mfma_kernel (4-bit)",
                 "ops_per_launch": 2 * head_step.macs}
     out = {
         "metric": "GMAC/s per qconv layer at INT8/4/2/1 (batch), % of int8 MFMA peak",

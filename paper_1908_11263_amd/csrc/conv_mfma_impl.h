@@ -269,7 +269,7 @@ __device__ __forceinline__ TileXY tile_xy(const ConvArgs &a, int tile)
 }
 
 template <int BITS, int MR, int NC, bool AL16>
-__global__ void __launch_bounds__(256) conv_mfma_kernel(ConvArgs a)
+__global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
 {
     extern __shared__ __align__(16) uint8_t smem[];
     constexpr int MT = 16 * MR;

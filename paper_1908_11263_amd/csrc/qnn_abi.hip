@@ -158,6 +158,8 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
     int64_t best_units = -1;
     for (int cmr = mr_first; cmr >= 1; cmr >>= 1) {
         for (int cnc = 4; cnc >= 1; cnc >>= 1) {
+            if (cmr * cnc > 8)
+                continue;  // 64 x 256 tiles exceed the register budget of two workgroups per CU
             const int MT = 16 * cmr, PT = 64 * cnc;
             ConvArgs c = a;
             int ti, th, tw;
