@@ -37,51 +37,39 @@ namespace qnn {
 
 typedef int32_t v4i __attribute__((ext_vector_type(4)));
 
-// Four 4-bit two's complement weights (16 bits, lowest element in the low
-// nibble) -> four bytes holding 16*w each.
-__device__ __forceinline__ uint32_t w4_to_s8x16(uint32_t u)
-{
-    return ((u & 0xFu) << 4) | ((u & 0xF0u) << 8) | ((u & 0xF00u) << 12) | ((u & 0xF000u) << 16);
-}
+// Sub-byte K order.  Within each packed 32-bit word (8 INT-4 or 16 INT-2
+// codes, lowest channel in the lowest bits) the unpacked bytes are stored
+// field-major: INT-4 word -> [c0 c2 c4 c6 | c1 c3 c5 c7], INT-2 word ->
+// [c0 c4 c8 c12 | c1 c5 c9 c13 | c2 ... | c3 ... c15].  Weights and
+// activations use the same order at the same K positions (packed words of a
+// filter row and of a pixel both start at multiples of 8 / 16 channels), so
+// every dot product is unchanged, and each unpack is a mask and a shift.
 
-// Four 2-bit two's complement weights (one byte) -> four bytes holding 64*w.
-__device__ __forceinline__ uint32_t w2_to_s8x64(uint32_t u)
-{
-    return ((u & 0x3u) << 6) | ((u & 0xCu) << 12) | ((u & 0x30u) << 18) | ((u & 0xC0u) << 24);
-}
-
-// Eight unsigned 4-bit activations -> eight bytes (natural order).
-__device__ __forceinline__ uint2 a4_to_u8(uint32_t v)
-{
-    uint2 r;
-    r.x = (v & 0xFu) | ((v & 0xF0u) << 4) | ((v & 0xF00u) << 8) | ((v & 0xF000u) << 12);
-    v >>= 16;
-    r.y = (v & 0xFu) | ((v & 0xF0u) << 4) | ((v & 0xF00u) << 8) | ((v & 0xF000u) << 12);
-    return r;
-}
-
-// Four unsigned 2-bit activations (one byte) -> four bytes.
-__device__ __forceinline__ uint32_t a2_byte_to_u8(uint32_t u)
-{
-    return (u & 0x3u) | ((u & 0xCu) << 6) | ((u & 0x30u) << 12) | ((u & 0xC0u) << 18);
-}
-
-// Stage one packed 4-byte word of activations at `dst` (unpacked bytes).
+// Activations, one packed word -> 4 (INT-8, offset by -128), 8 or 16 bytes.
 template <int BITS>
 __device__ __forceinline__ void stage_word(uint8_t *dst, uint32_t v)
 {
     if (BITS == 8) {
         *(uint32_t *)dst = v ^ 0x80808080u;
     } else if (BITS == 4) {
-        *(uint2 *)dst = a4_to_u8(v);
+        *(uint2 *)dst = make_uint2(v & 0x0F0F0F0Fu, (v >> 4) & 0x0F0F0F0Fu);
     } else {
-        uint4 o;
-        o.x = a2_byte_to_u8(v & 0xFFu);
-        o.y = a2_byte_to_u8((v >> 8) & 0xFFu);
-        o.z = a2_byte_to_u8((v >> 16) & 0xFFu);
-        o.w = a2_byte_to_u8(v >> 24);
-        *(uint4 *)dst = o;
+        *(uint4 *)dst = make_uint4(v & 0x03030303u, (v >> 2) & 0x03030303u, (v >> 4) & 0x03030303u,
+                                   (v >> 6) & 0x03030303u);
     }
+}
+
+// Weights, one packed word -> 8 (INT-4) or 16 (INT-2) bytes holding 16*w /
+// 64*w: the code moved to the top of its byte is exactly that signed byte.
+__device__ __forceinline__ uint2 w4_word(uint32_t v)
+{
+    return make_uint2((v << 4) & 0xF0F0F0F0u, v & 0xF0F0F0F0u);
+}
+
+__device__ __forceinline__ uint4 w2_word(uint32_t v)
+{
+    return make_uint4((v << 6) & 0xC0C0C0C0u, (v << 4) & 0xC0C0C0C0u, (v << 2) & 0xC0C0C0C0u,
+                      v & 0xC0C0C0C0u);
 }
 
 __device__ __forceinline__ int wave_sum(int s)
@@ -100,36 +88,22 @@ __device__ __forceinline__ int64_t round_shift(int64_t t, int s)
     return s == 0 ? t : (t >> s) + ((t >> (s - 1)) & 1);
 }
 
-// Stage 16 packed weight bytes (natural order) as int8 at dst: 16, 32 or 64
-// bytes for 8, 4, 2 bits (4-/2-bit codes scaled by 16 / 64).
+// Stage 16 packed weight bytes as int8 at dst: 16, 32 or 64 bytes for 8, 4,
+// 2 bits, in the sub-byte K order above.
 template <int BITS>
 __device__ __forceinline__ void stage_w16(int8_t *dst, uint4 v)
 {
     if (BITS == 8) {
         *(uint4 *)dst = v;
     } else if (BITS == 4) {
-        uint4 o0, o1;
-        o0.x = w4_to_s8x16(v.x & 0xFFFFu);
-        o0.y = w4_to_s8x16(v.x >> 16);
-        o0.z = w4_to_s8x16(v.y & 0xFFFFu);
-        o0.w = w4_to_s8x16(v.y >> 16);
-        o1.x = w4_to_s8x16(v.z & 0xFFFFu);
-        o1.y = w4_to_s8x16(v.z >> 16);
-        o1.z = w4_to_s8x16(v.w & 0xFFFFu);
-        o1.w = w4_to_s8x16(v.w >> 16);
-        *(uint4 *)dst = o0;
-        *(uint4 *)(dst + 16) = o1;
+        const uint2 a = w4_word(v.x), b = w4_word(v.y), c = w4_word(v.z), d = w4_word(v.w);
+        *(uint4 *)dst = make_uint4(a.x, a.y, b.x, b.y);
+        *(uint4 *)(dst + 16) = make_uint4(c.x, c.y, d.x, d.y);
     } else {
-        const uint32_t d[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            uint4 o;
-            o.x = w2_to_s8x64(d[i] & 0xFFu);
-            o.y = w2_to_s8x64((d[i] >> 8) & 0xFFu);
-            o.z = w2_to_s8x64((d[i] >> 16) & 0xFFu);
-            o.w = w2_to_s8x64(d[i] >> 24);
-            *(uint4 *)(dst + 16 * i) = o;
-        }
+        *(uint4 *)dst = w2_word(v.x);
+        *(uint4 *)(dst + 16) = w2_word(v.y);
+        *(uint4 *)(dst + 32) = w2_word(v.z);
+        *(uint4 *)(dst + 48) = w2_word(v.w);
     }
 }
 
@@ -141,6 +115,7 @@ __device__ __forceinline__ void stage_w16(int8_t *dst, uint4 v)
 // mult fit 24 bits this is exact with one 24-bit multiply-add per output if
 // R + D * mult < 2^32 (mode 1), else with a 32x32->64 multiply-add (mode 2);
 // other channels use the direct 64-bit form.  Two 16-byte words per channel:
+//   mode 3:     e0 = {S t_lo, S D, mult, S n0}, e1 = {shift + log2 S, 0, 3, 0}
 //   modes 1, 2: e0 = {a_base, D, mult, R}, e1 = {Q, shift, mode, 0}
 //   direct:     e0 = {bias lo, bias hi, mult, shift}, e1 = {0, 0, 0, 0}
 // (RAW32 uses the slow word's bias only.)
@@ -158,7 +133,8 @@ __device__ __forceinline__ int64_t floor_div_pos(int64_t a, int64_t b)
 }
 
 __device__ __forceinline__ void requant_plan(int64_t bias, int32_t mult, int32_t shift, int32_t lo,
-                                             int32_t hi, bool requant, int4 &e0, int4 &e1)
+                                             int32_t hi, bool requant, int scale_log2, int4 &e0,
+                                             int4 &e1)
 {
     e0 = make_int4((int32_t)(uint32_t)(uint64_t)bias, (int32_t)(bias >> 32), mult, shift);
     e1 = make_int4(0, 0, 0, 0);
@@ -169,6 +145,23 @@ __device__ __forceinline__ void requant_plan(int64_t bias, int32_t mult, int32_t
     // smallest accumulator whose code reaches p: ceil((p 2^s - half) / mult) - bias
     const int64_t t_lo = -floor_div_pos(half - (int64_t)lo * two_s, mult) - bias;
     const int64_t t_hi = -floor_div_pos(half - (int64_t)hi * two_s, mult) - bias;
+    // Strict form (mode 3): with mult <= 2^shift the code rises by at most one
+    // per accumulator unit, so it is exactly lo at t_lo and hi at t_hi and
+    //   code = (clamp(acc' - S t_lo, 0, S D) * mult + S n0) >> (shift + log2 S)
+    // on the scaled accumulator acc' = S acc (S = 16 / 64 for 4 / 2 bits), where
+    // n0 = (t_lo + bias) mult + 2^(shift-1) = lo 2^shift + R, 0 <= R < 2^shift.
+    if (mult <= two_s && lo >= 0 && shift + scale_log2 <= 31) {
+        const int64_t S = (int64_t)1 << scale_log2;
+        const int64_t Dn = t_hi - t_lo;
+        const int64_t n0s = (t_lo + bias) * (int64_t)mult + half;
+        const int64_t A = S * t_lo;
+        if (A >= INT32_MIN && A <= INT32_MAX && Dn >= 0 && S * Dn < (1 << 24) && mult < (1 << 24) &&
+            n0s >= 0 && S * (n0s + Dn * (int64_t)mult) < ((int64_t)1 << 32)) {
+            e0 = make_int4((int32_t)A, (int32_t)(S * Dn), mult, (int32_t)(uint32_t)(S * n0s));
+            e1 = make_int4(shift + scale_log2, 0, 3, 0);
+            return;
+        }
+    }
     const int64_t a_base = t_lo - 1;
     const int64_t D = t_hi - a_base;
     if (a_base < INT32_MIN || t_hi > INT32_MAX || D < 0 || D >= (1 << 24) || mult >= (1 << 24))
@@ -290,13 +283,16 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
 
     // ---- prologue: every independent load is issued before any is used ----
     // per-channel epilogue parameters (one thread per channel)
+    // (channel ch = wave + 4 * lane, so every wave computes a quarter of the plans)
+    const int pch = wv + 4 * lane;
+    const bool has_ch = lane < MT / 4;
     int32_t p_bias = 0, p_mult = 0, p_shift = 0;
-    if (tid < MT && m0 + tid < a.m) {
+    if (has_ch && m0 + pch < a.m) {
         if (a.bias)
-            p_bias = a.bias[m0 + tid];
+            p_bias = a.bias[m0 + pch];
         if (a.epi == EPI_REQUANT) {
-            p_mult = a.mult[m0 + tid];
-            p_shift = a.shift[m0 + tid];
+            p_mult = a.mult[m0 + pch];
+            p_shift = a.shift[m0 + pch];
         }
     }
     // filter tile, first batch (contiguous rows, natural order = chunk order)
@@ -406,12 +402,18 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                 if (idx < nit && mg < a.m && 4 * d < sVld[j]) {
                     const uint8_t *wr = a.w + (size_t)mg * a.wrow;
                     const int e = sNat[j] + 4 * d;
-                    if (BITS == 8)
+                    if (BITS == 8) {
                         v[u] = *(const uint32_t *)(wr + e);
-                    else if (BITS == 4)
-                        v[u] = *(const uint16_t *)(wr + (e >> 1));
-                    else
-                        v[u] = wr[e >> 2];
+                    } else if (BITS == 4) {
+                        // bytes e..e+3 of the K order are one half of packed word e / 8
+                        const uint2 h = w4_word(*(const uint32_t *)(wr + ((e >> 3) << 2)));
+                        v[u] = (e & 4) ? h.y : h.x;
+                    } else {
+                        // bytes e..e+3 are field (e / 4) % 4 of packed word e / 16
+                        const uint4 f = w2_word(*(const uint32_t *)(wr + ((e >> 4) << 2)));
+                        const int k = (e >> 2) & 3;
+                        v[u] = k == 0 ? f.x : (k == 1 ? f.y : (k == 2 ? f.z : f.w));
+                    }
                 }
             }
 #pragma unroll
@@ -420,12 +422,7 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                 if (idx < nit) {
                     const int row = (int)fdiv((uint32_t)idx, a.div_ncol);
                     const int col = idx - row * ncol;
-                    uint32_t val = v[u];
-                    if (BITS == 4)
-                        val = w4_to_s8x16(val);
-                    else if (BITS == 2)
-                        val = w2_to_s8x64(val);
-                    *(uint32_t *)(sW + row * a.kp + col * 4) = val;
+                    *(uint32_t *)(sW + row * a.kp + col * 4) = v[u];
                 }
             }
         }
@@ -457,32 +454,39 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
         }
         __syncthreads();
     }
-    int mode = 1;
-    if (tid < MT) {
-        int64_t b = p_bias;
-        if (BITS == 8)
-            b += 128 * (int64_t)sWsum[tid];
-        p_shift = p_shift < 0 ? 0 : (p_shift > 62 ? 62 : p_shift);
+    constexpr int SL = BITS == 4 ? 4 : (BITS == 2 ? 6 : 0);  // log2 of the weight scale
+    int mode = 0;
+    if (has_ch) {
         int4 e0, e1;
-        requant_plan(b, p_mult, p_shift, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, e0, e1);
-        if (m0 + tid >= a.m)
-            e1.z = 1;  // missing channels: code forced to 0 below
-        sEpi[2 * tid] = e0;
-        sEpi[2 * tid + 1] = e1;
+        if (m0 + pch < a.m) {
+            int64_t b = p_bias;
+            if (BITS == 8)
+                b += 128 * (int64_t)sWsum[pch];
+            p_shift = p_shift < 0 ? 0 : (p_shift > 62 ? 62 : p_shift);
+            requant_plan(b, p_mult, p_shift, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, SL, e0, e1);
+        } else {
+            // missing channel: a strict plan that yields code 0 (and RAW32 skips it)
+            e0 = make_int4(0, 0, 0, 0);
+            e1 = make_int4(0, 0, 3, 0);
+        }
+        sEpi[2 * pch] = e0;
+        sEpi[2 * pch + 1] = e1;
         mode = e1.z;
     }
     // workgroup-uniform epilogue selection: per-wave votes in LDS, then the
     // barrier that also publishes sEpi
     {
-        const bool v32 = __all(mode == 1);
-        const bool v64 = __all(mode == 1 || mode == 2);
+        const bool v3 = __all(!has_ch || mode == 3);
+        const bool v32 = __all(!has_ch || mode == 1);
+        const bool v64 = __all(!has_ch || mode == 1 || mode == 2);
         if (lane == 0)
-            sWsum[MT + wv] = (v32 ? 1 : 0) | (v64 ? 2 : 0);
+            sWsum[MT + wv] = (v32 ? 1 : 0) | (v64 ? 2 : 0) | (v3 ? 4 : 0);
     }
     __syncthreads();
     const int votes = sWsum[MT] & sWsum[MT + 1] & sWsum[MT + 2] & sWsum[MT + 3];
-    const bool all32 = (votes & 1) != 0;
-    const bool all64 = (votes & 2) != 0;
+    const bool all3 = (votes & 4) != 0;
+    const bool all32 = (votes & 1) != 0 && !all3;
+    const bool all64 = (votes & 2) != 0 && !all3;
     const bool full = m0 + MT <= a.m;
 
     const int tile_px = a.ti * a.th * a.tw;
@@ -602,7 +606,29 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
                     packed[t][c] = 0;
-            if (all32 || all64) {
+            if (all3) {
+                // strict plan: code = (clamp(acc' - A, 0, DS) * mult + RS) >> shift'
+#pragma unroll
+                for (int t = 0; t < MR; ++t) {
+                    int4 e0[4], e1[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        e0[i] = sEpi[2 * (t * 16 + 4 * g + i)];
+                        e1[i] = sEpi[2 * (t * 16 + 4 * g + i) + 1];
+                    }
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+#pragma unroll
+                        for (int c = 0; c < NC; ++c) {
+                            const int32_t d = __builtin_elementwise_sub_sat((int32_t)acc[t][c][i], e0[i].x);
+                            const uint32_t dc = (uint32_t)min(max(d, 0), e0[i].y);
+                            const uint32_t code = (__umul24(dc, (uint32_t)e0[i].z) + (uint32_t)e0[i].w) >> e1[i].x;
+                            packed[t][c] |= code << (i * BITS);
+                        }
+                    }
+                    __builtin_amdgcn_sched_barrier(0);
+                }
+            } else if (all32 || all64) {
                 // plan form: code = clip(Q + ((clamp(acc - a_base, 0, D) * mult + R) >> shift))
 #pragma unroll
                 for (int t = 0; t < MR; ++t) {
@@ -652,6 +678,12 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                         const int4 e1 = sEpi[2 * mrow + 1];
 #pragma unroll
                         for (int c = 0; c < NC; ++c) {
+                            if (e1.z == 3) {
+                                const int32_t d = __builtin_elementwise_sub_sat((int32_t)acc[t][c][i], e0.x);
+                                const uint32_t dc = (uint32_t)min(max(d, 0), e0.y);
+                                packed[t][c] |= ((__umul24(dc, (uint32_t)e0.z) + (uint32_t)e0.w) >> e1.x) << (i * BITS);
+                                continue;
+                            }
                             int32_t acc32 = acc[t][c][i];
                             if (BITS == 4)
                                 acc32 >>= 4;
@@ -692,7 +724,22 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
         __syncthreads();
 
         // ---- coalesced copy of the packed output tile ----
-        if (a.epi != EPI_RAW32) {
+        if (a.epi != EPI_RAW32 && a.contig) {
+            // the tile's valid pixels are consecutive output pixels and the tile
+            // holds every channel: one flat copy
+            const int valid = a.ti == 1 ? min(a.th, a.ho - T.oy0) * a.wo
+                                        : min(a.ti, a.n - T.n0) * a.ho * a.wo;
+            const size_t first = a.ti == 1 ? ((size_t)T.n0 * a.ho + T.oy0) * a.wo : (size_t)T.n0 * a.ho * a.wo;
+            uint8_t *dst = a.y + first * a.ypb;
+            const int nbytes = valid * a.ypb;
+            if ((a.ypb & 15) == 0) {
+                for (int o = tid * 16; o < nbytes; o += 256 * 16)
+                    *(uint4 *)(dst + o) = *(const uint4 *)(sOut + o);
+            } else {
+                for (int o = tid * 4; o < nbytes; o += 256 * 4)
+                    *(uint32_t *)(dst + o) = *(const uint32_t *)(sOut + o);
+            }
+        } else if (a.epi != EPI_RAW32) {
             const int ob0 = m0 * BITS / 8;
             const int obn = min(a.ot_b, a.ypb - ob0);
             const int tq4 = tile_px * a.obq;

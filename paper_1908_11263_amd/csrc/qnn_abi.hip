@@ -344,6 +344,8 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
         a.obq = 1;
     }
     a.div_obq = make_fastdiv((uint32_t)a.obq);
+    a.contig = a.epi == EPI_REQUANT && a.tw == a.wo && (a.ti == 1 || a.th == a.ho) &&
+               a.ot_b == ypb && (ypb % 4) == 0 && m <= 16 * mr;
     a.div_qrow = make_fastdiv((uint32_t)(a.wrow / 16 > 0 ? a.wrow / 16 : 1));
     a.div_ncol = make_fastdiv((uint32_t)(16 * a.ksteps));
     st = device_info(&cus);

@@ -63,6 +63,7 @@ struct ConvArgs {
     FastDiv div_ncol;      // 4-byte words per staged filter row
     int32_t pbq, quad16;   // quads per pixel, 1 if the quad is 16 bytes else 4 bytes
     int32_t ob0, obn, obq, oquad16;  // copy-out byte offset, byte count, quads, quad size flag
+    int32_t contig;        // tile = consecutive output pixels with every channel: flat copy-out
 };
 
 // Arguments of the INT-1 XNOR/popcount convolution.
