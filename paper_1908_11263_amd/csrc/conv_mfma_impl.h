@@ -115,7 +115,8 @@ __device__ __forceinline__ void stage_w16(int8_t *dst, uint4 v)
 // mult fit 24 bits this is exact with one 24-bit multiply-add per output if
 // R + D * mult < 2^32 (mode 1), else with a 32x32->64 multiply-add (mode 2);
 // other channels use the direct 64-bit form.  Two 16-byte words per channel:
-//   mode 3:     e0 = {S t_lo, S D, mult, S n0}, e1 = {shift + log2 S, 0, 3, 0}
+//   modes 3, 4: e0 = {S t_lo, S D, mult, S n0 lo}, e1 = {shift + log2 S, S n0 hi, mode, 0}
+//               (mode 3 when the expression fits 32 bits, mode 4 with a 64-bit product)
 //   modes 1, 2: e0 = {a_base, D, mult, R}, e1 = {Q, shift, mode, 0}
 //   direct:     e0 = {bias lo, bias hi, mult, shift}, e1 = {0, 0, 0, 0}
 // (RAW32 uses the slow word's bias only.)
@@ -145,7 +146,7 @@ __device__ __forceinline__ void requant_plan(int64_t bias, int32_t mult, int32_t
     // smallest accumulator whose code reaches p: ceil((p 2^s - half) / mult) - bias
     const int64_t t_lo = -floor_div_pos(half - (int64_t)lo * two_s, mult) - bias;
     const int64_t t_hi = -floor_div_pos(half - (int64_t)hi * two_s, mult) - bias;
-    // Strict form (mode 3): with mult <= 2^shift the code rises by at most one
+    // Strict form (modes 3, 4): with mult <= 2^shift the code rises by at most one
     // per accumulator unit, so it is exactly lo at t_lo and hi at t_hi and
     //   code = (clamp(acc' - S t_lo, 0, S D) * mult + S n0) >> (shift + log2 S)
     // on the scaled accumulator acc' = S acc (S = 16 / 64 for 4 / 2 bits), where
@@ -156,9 +157,12 @@ __device__ __forceinline__ void requant_plan(int64_t bias, int32_t mult, int32_t
         const int64_t n0s = (t_lo + bias) * (int64_t)mult + half;
         const int64_t A = S * t_lo;
         if (A >= INT32_MIN && A <= INT32_MAX && Dn >= 0 && S * Dn < (1 << 24) && mult < (1 << 24) &&
-            n0s >= 0 && S * (n0s + Dn * (int64_t)mult) < ((int64_t)1 << 32)) {
-            e0 = make_int4((int32_t)A, (int32_t)(S * Dn), mult, (int32_t)(uint32_t)(S * n0s));
-            e1 = make_int4(shift + scale_log2, 0, 3, 0);
+            n0s >= 0 && S * (n0s + Dn * (int64_t)mult) < ((int64_t)1 << 62)) {
+            const int64_t rs = S * n0s;
+            // mode 3: the whole expression fits 32 bits; mode 4: 64-bit multiply-add
+            const int md = S * (n0s + Dn * (int64_t)mult) < ((int64_t)1 << 32) ? 3 : 4;
+            e0 = make_int4((int32_t)A, (int32_t)(S * Dn), mult, (int32_t)(uint32_t)rs);
+            e1 = make_int4(shift + scale_log2, (int32_t)(rs >> 32), md, 0);
             return;
         }
     }
@@ -477,14 +481,16 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
     // barrier that also publishes sEpi
     {
         const bool v3 = __all(!has_ch || mode == 3);
+        const bool v4 = __all(!has_ch || mode == 3 || mode == 4);
         const bool v32 = __all(!has_ch || mode == 1);
         const bool v64 = __all(!has_ch || mode == 1 || mode == 2);
         if (lane == 0)
-            sWsum[MT + wv] = (v32 ? 1 : 0) | (v64 ? 2 : 0) | (v3 ? 4 : 0);
+            sWsum[MT + wv] = (v32 ? 1 : 0) | (v64 ? 2 : 0) | (v3 ? 4 : 0) | (v4 ? 8 : 0);
     }
     __syncthreads();
     const int votes = sWsum[MT] & sWsum[MT + 1] & sWsum[MT + 2] & sWsum[MT + 3];
     const bool all3 = (votes & 4) != 0;
+    const bool all4 = (votes & 8) != 0 && !all3;
     const bool all32 = (votes & 1) != 0 && !all3;
     const bool all64 = (votes & 2) != 0 && !all3;
     const bool full = m0 + MT <= a.m;
@@ -492,15 +498,16 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
     const int tile_px = a.ti * a.th * a.tw;
     const int g = lane >> 4, r16 = lane & 15;
 
-    for (bool first = true; tile < a.ntiles; tile += gridDim.x, first = false) {
-        if (!first) {
-            T = tile_xy(a, tile);
-            if (a.quad16)
-                halo_stage_from<BITS, true, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
-            else
-                halo_stage_from<BITS, false, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
-            __syncthreads();
-        }
+    for (; tile < a.ntiles; tile += gridDim.x) {
+        // the next tile's first input batch is loaded into registers now and
+        // lands in LDS after this tile's MFMAs and epilogue, so its latency
+        // hides behind them
+        const int next = tile + gridDim.x;
+        TileXY Tn = tile_xy(a, next < a.ntiles ? next : tile);
+        if (a.quad16)
+            halo_issue<BITS, true, UH>(a, tid, next < a.ntiles ? totq : 0, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
+        else
+            halo_issue<BITS, false, UH>(a, tid, next < a.ntiles ? totq : 0, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
 
         // ---- main loop: MR x NC MFMA tiles per 64-deep K step ----
         int base[NC];
@@ -560,6 +567,12 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                 bv[c] = bn[c];
         }
 
+        // the plan reads below do not depend on the tile; an opaque zero keeps
+        // the compiler from hoisting all of them out of the tile loop (which
+        // would hold every channel's plan in registers)
+        int ez = 0;
+        __asm__ volatile("" : "+v"(ez));
+        const int4 *ep = sEpi + ez;
         // ---- epilogue: lane (r16, g) of tile (t, c) holds channels
         // t*16 + 4g + {0..3} of pixel c*16 + r16 of its wave ----
         int gpix[NC];
@@ -582,10 +595,10 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
             for (int t = 0; t < MR; ++t)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const int mrow = t * 16 + 4 * g + i;
+                    const int mrow = t * 16 + 4 * g + i + ez;
                     if (m0 + mrow >= a.m)
                         continue;
-                    const int4 e0 = sEpi[2 * mrow];
+                    const int4 e0 = ep[2 * mrow];
                     const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);
 #pragma unroll
                     for (int c = 0; c < NC; ++c) {
@@ -606,15 +619,15 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
                     packed[t][c] = 0;
-            if (all3) {
+            if (all3 || all4) {
                 // strict plan: code = (clamp(acc' - A, 0, DS) * mult + RS) >> shift'
 #pragma unroll
                 for (int t = 0; t < MR; ++t) {
                     int4 e0[4], e1[4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        e0[i] = sEpi[2 * (t * 16 + 4 * g + i)];
-                        e1[i] = sEpi[2 * (t * 16 + 4 * g + i) + 1];
+                        e0[i] = ep[2 * (t * 16 + 4 * g + i + ez)];
+                        e1[i] = ep[2 * (t * 16 + 4 * g + i + ez) + 1];
                     }
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
@@ -622,7 +635,13 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                         for (int c = 0; c < NC; ++c) {
                             const int32_t d = __builtin_elementwise_sub_sat((int32_t)acc[t][c][i], e0[i].x);
                             const uint32_t dc = (uint32_t)min(max(d, 0), e0[i].y);
-                            const uint32_t code = (__umul24(dc, (uint32_t)e0[i].z) + (uint32_t)e0[i].w) >> e1[i].x;
+                            uint32_t code;
+                            if (all3) {
+                                code = (__umul24(dc, (uint32_t)e0[i].z) + (uint32_t)e0[i].w) >> e1[i].x;
+                            } else {
+                                const uint64_t rs = ((uint64_t)(uint32_t)e1[i].y << 32) | (uint32_t)e0[i].w;
+                                code = (uint32_t)(((uint64_t)dc * (uint32_t)e0[i].z + rs) >> e1[i].x);
+                            }
                             packed[t][c] |= code << (i * BITS);
                         }
                     }
@@ -635,12 +654,12 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                     int4 e0[4], e1[4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        e0[i] = sEpi[2 * (t * 16 + 4 * g + i)];
-                        e1[i] = sEpi[2 * (t * 16 + 4 * g + i) + 1];
+                        e0[i] = ep[2 * (t * 16 + 4 * g + i + ez)];
+                        e1[i] = ep[2 * (t * 16 + 4 * g + i + ez) + 1];
                     }
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const bool live = full || (m0 + t * 16 + 4 * g + i < a.m);
+                        const bool live = full || (m0 + t * 16 + 4 * g + i + ez < a.m);
 #pragma unroll
                         for (int c = 0; c < NC; ++c) {
                             int32_t acc32 = acc[t][c][i];
@@ -671,17 +690,18 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                 for (int t = 0; t < MR; ++t)
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        const int mrow = t * 16 + 4 * g + i;
+                        const int mrow = t * 16 + 4 * g + i + ez;
                         if (m0 + mrow >= a.m)
                             continue;
-                        const int4 e0 = sEpi[2 * mrow];
-                        const int4 e1 = sEpi[2 * mrow + 1];
+                        const int4 e0 = ep[2 * mrow];
+                        const int4 e1 = ep[2 * mrow + 1];
 #pragma unroll
                         for (int c = 0; c < NC; ++c) {
-                            if (e1.z == 3) {
+                            if (e1.z >= 3) {
                                 const int32_t d = __builtin_elementwise_sub_sat((int32_t)acc[t][c][i], e0.x);
                                 const uint32_t dc = (uint32_t)min(max(d, 0), e0.y);
-                                packed[t][c] |= ((__umul24(dc, (uint32_t)e0.z) + (uint32_t)e0.w) >> e1.x) << (i * BITS);
+                                const uint64_t rs = ((uint64_t)(uint32_t)e1.y << 32) | (uint32_t)e0.w;
+                                packed[t][c] |= (uint32_t)(((uint64_t)dc * (uint32_t)e0.z + rs) >> e1.x) << (i * BITS);
                                 continue;
                             }
                             int32_t acc32 = acc[t][c][i];
@@ -764,6 +784,20 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                 }
             }
         }
+        // every wave is past this tile's MFMAs (barrier above): the next input
+        // tile may overwrite sX; the barrier below also keeps the next
+        // epilogue from overwriting sOut before this copy-out is done
+        if (next < a.ntiles) {
+            if (a.quad16) {
+                halo_store<BITS, true, UH>(sX, hq, hd);
+                halo_stage_from<BITS, true, UH>(a, sX, tid + 256 * UH, Tn.n0, Tn.iy0, Tn.ix0);
+            } else {
+                halo_store<BITS, false, UH>(sX, hq, hd);
+                halo_stage_from<BITS, false, UH>(a, sX, tid + 256 * UH, Tn.n0, Tn.iy0, Tn.ix0);
+            }
+        }
+        T = Tn;
+        __syncthreads();
     }
 }
 

@@ -120,38 +120,112 @@ qnn_status check_epi(const qnn_epi *e, int bits, int32_t m)
     return QNN_OK;
 }
 
-// Tile planning for the MFMA convolution.  Returns QNN_ERR_UNSUPPORTED when no
-// tile fits the local memory of a compute unit.
-qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
+// Fits an output tile of PT pixels and MT channels: fills the tile geometry,
+// LDS offsets and tile counts of `c`; returns the LDS bytes, or -1.
+int64_t fit_tile(ConvArgs &c, int MT, int PT, int bits, int obits, int64_t w_bytes, int64_t tab_bytes,
+                 bool code_staging, bool alias = false)
+{
+    int ti, th, tw;
+    if ((int64_t)c.ho * c.wo >= PT) {
+        ti = 1;
+        tw = c.wo < PT ? c.wo : PT;
+        th = PT / tw;
+        if (th > c.ho)
+            th = c.ho;
+    } else {
+        ti = PT / (c.ho * c.wo);
+        if (ti > c.n)
+            ti = c.n > 0 ? c.n : 1;
+        th = c.ho;
+        tw = c.wo;
+    }
+    const int hh = (th - 1) * c.sh + c.kh;
+    const int hwd = (tw - 1) * c.sw + c.kw;
+    const int64_t x_bytes = (int64_t)ti * hh * hwd * c.ps + 64;
+    const int ot_b = obits == 32 ? 0 : MT * bits / 8;
+    // output staging: the packed tile, or one byte per code with a pixel
+    // stride of MT + 16 (the two pixel groups a wave writes at once, 4 pixels
+    // apart, then fall in different LDS banks)
+    const int cs = obits == 32 ? 0 : (code_staging ? MT + 16 : ot_b);
+    const int64_t o_bytes = (int64_t)PT * cs;
+    int64_t off = w_bytes;
+    off = (off + 15) & ~(int64_t)15;
+    const int64_t off_tab = off;
+    off += tab_bytes;
+    off = (off + 15) & ~(int64_t)15;
+    const int64_t off_wsum = off;
+    off += 4 * MT + 16 + 32 * MT;   // filter sums, votes, requantization plans
+    off = (off + 15) & ~(int64_t)15;
+    const int64_t off_x = off;
+    off += (x_bytes + 15) & ~(int64_t)15;
+    // the output staging either follows the input tile or, when asked for
+    // and small enough, reuses it (the kernel then separates the two uses
+    // with barriers)
+    const bool share = alias && o_bytes <= x_bytes;
+    if (alias && !share)
+        return -1;
+    const int64_t off_out = share ? off_x : off;
+    if (!share)
+        off += o_bytes;
+    if (off > kLdsBytes)
+        return -1;
+    c.ti = ti;
+    c.th = th;
+    c.tw = tw;
+    c.hh = hh;
+    c.hwd = hwd;
+    c.ot_b = ot_b;
+    c.cs = cs;
+    c.alias_out = share ? 1 : 0;
+    c.off_tab = (int32_t)off_tab;
+    c.off_wsum = (int32_t)off_wsum;
+    c.off_x = (int32_t)off_x;
+    c.off_out = (int32_t)off_out;
+    c.lds_bytes = (int32_t)off;
+    c.tiles_x = (c.wo + tw - 1) / tw;
+    c.tiles_y = (c.ho + th - 1) / th;
+    const int64_t tiles_n = (c.n + ti - 1) / ti;
+    const int64_t nt = tiles_n * c.tiles_y * c.tiles_x;
+    if (nt > (int64_t)1 << 30)
+        return -1;
+    c.ntiles = (int32_t)nt;
+    return off;
+}
+
+// K walk common to both kernels: 16-byte K chunks, tap by tap when a pixel
+// is a whole number of chunks, else along each filter row.
+void plan_k_walk(ConvArgs &a, int &al16)
 {
     const int c8 = a.c8;
     a.row_mode = (c8 % 16) != 0;
-    int kchunks, ps;
     if (a.row_mode) {
         a.row_len = a.kw * c8;
         a.cpr = (a.row_len + 15) / 16;
-        kchunks = a.kh * a.cpr;
-        ps = c8;
+        a.kchunks = a.kh * a.cpr;
+        a.ps = c8;
     } else {
         a.row_len = 0;
         a.cpr = 0;
-        kchunks = a.kh * a.kw * (c8 / 16);
+        a.kchunks = a.kh * a.kw * (c8 / 16);
         // keep the pixel stride an odd multiple of 16 bytes, so 16 lanes
         // reading 16 neighbouring pixels hit 16 different bank groups
-        ps = ((c8 / 16) % 2 == 0) ? c8 + 16 : c8;
+        a.ps = ((c8 / 16) % 2 == 0) ? c8 + 16 : c8;
     }
-    a.kchunks = kchunks;
-    a.ksteps = (kchunks + 3) / 4;
-    a.kp = a.ksteps * 64 + 16;
-    a.ps = ps;
     al16 = a.row_mode ? 0 : 1;
-    const int obits = a.epi == EPI_REQUANT ? bits : 32;
-    const int64_t tab_bytes = 3 * 4 * (int64_t)(4 * a.ksteps);
+}
 
-    // Candidates in order of preference (widest channel tile, then widest
-    // pixel tile).  Take the first that fits the local memory and still gives
-    // at least two tiles per compute unit; if none does, the one with the most
-    // tiles (small layers are latency-bound and want parallelism).
+// 16x16x64 kernel: candidates in order of preference (widest channel tile,
+// then widest pixel tile); the first that fits the local memory and gives at
+// least two tiles per compute unit, else the one with the most tiles (small
+// layers are latency-bound and want parallelism).
+qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
+{
+    plan_k_walk(a, al16);
+    a.ksteps = (a.kchunks + 3) / 4;
+    a.kch = 4 * a.ksteps;
+    a.kp = a.ksteps * 64 + 16;
+    const int obits = a.epi == EPI_REQUANT ? bits : 32;
+    const int64_t tab_bytes = 3 * 4 * (int64_t)a.kch;
     const int mr_first = a.m <= 16 ? 1 : (a.m <= 32 ? 2 : 4);
     ConvArgs best = a;
     int best_mr = 0, best_nc = 0;
@@ -160,59 +234,10 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
         for (int cnc = 4; cnc >= 1; cnc >>= 1) {
             if (cmr * cnc > 8)
                 continue;  // 64 x 256 tiles exceed the register budget of two workgroups per CU
-            const int MT = 16 * cmr, PT = 64 * cnc;
             ConvArgs c = a;
-            int ti, th, tw;
-            if ((int64_t)c.ho * c.wo >= PT) {
-                ti = 1;
-                tw = c.wo < PT ? c.wo : PT;
-                th = PT / tw;
-                if (th > c.ho)
-                    th = c.ho;
-            } else {
-                ti = PT / (c.ho * c.wo);
-                if (ti > c.n)
-                    ti = c.n > 0 ? c.n : 1;
-                th = c.ho;
-                tw = c.wo;
-            }
-            const int hh = (th - 1) * c.sh + c.kh;
-            const int hwd = (tw - 1) * c.sw + c.kw;
-            const int64_t w_bytes = (int64_t)MT * c.kp;
-            const int64_t x_bytes = (int64_t)ti * hh * hwd * ps + 64;
-            const int ot_b = obits == 32 ? 0 : MT * bits / 8;
-            const int64_t o_bytes = (int64_t)PT * ot_b;
-            int64_t off = w_bytes;
-            const int64_t off_tab = off;
-            off += tab_bytes;
-            const int64_t off_wsum = off;
-            off += 4 * MT + 16 + 32 * MT;   // filter sums, votes, requantization plans
-            off = (off + 15) & ~(int64_t)15;
-            const int64_t off_x = off;
-            off += (x_bytes + 15) & ~(int64_t)15;
-            const int64_t off_out = off;
-            off += o_bytes;
-            if (off > kLdsBytes)
+            if (fit_tile(c, 16 * cmr, 64 * cnc, bits, obits, (int64_t)16 * cmr * a.kp, tab_bytes, false) < 0)
                 continue;
-            c.ti = ti;
-            c.th = th;
-            c.tw = tw;
-            c.hh = hh;
-            c.hwd = hwd;
-            c.ot_b = ot_b;
-            c.off_tab = (int32_t)off_tab;
-            c.off_wsum = (int32_t)off_wsum;
-            c.off_x = (int32_t)off_x;
-            c.off_out = (int32_t)off_out;
-            c.lds_bytes = (int32_t)off;
-            c.tiles_x = (c.wo + tw - 1) / tw;
-            c.tiles_y = (c.ho + th - 1) / th;
-            const int64_t tiles_n = (c.n + ti - 1) / ti;
-            const int64_t nt = tiles_n * c.tiles_y * c.tiles_x;
-            if (nt > (int64_t)1 << 30)
-                continue;
-            c.ntiles = (int32_t)nt;
-            const int64_t units = nt * ((c.m + MT - 1) / MT);
+            const int64_t units = (int64_t)c.ntiles * ((c.m + 16 * cmr - 1) / (16 * cmr));
             if (units >= 2 * kPlanCus) {
                 a = c;
                 mr = cmr;
@@ -233,6 +258,57 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
     mr = best_mr;
     nc = best_nc;
     return QNN_OK;
+}
+
+// 32x32x32 kernel with packed filters in LDS: used when the layer has at
+// least 32 output channels and enough tiles for two per compute unit; the
+// preferred tile keeps two workgroups per compute unit in the local memory.
+qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16)
+{
+    if (a.m < 32)
+        return QNN_ERR_UNSUPPORTED;
+    ConvArgs b = a;
+    plan_k_walk(b, al16);
+    // measured per layer: the 32x32 kernel wins every layer except 8-bit ones
+    // with a K walk along filter rows (pixels of less than 16 bytes)
+    if (bits == 8 && b.row_mode)
+        return QNN_ERR_UNSUPPORTED;
+    b.ksteps = 2 * ((b.kchunks + 3) / 4);  // an even number of 32-deep steps
+    b.kch = 2 * b.ksteps;
+    const int cb = 2 * bits;         // packed bytes per 16-byte K chunk
+    b.kp = (b.kch + 1) * cb;         // odd multiple of cb: conflict-free fragment reads
+    const int obits = b.epi == EPI_REQUANT ? bits : 32;
+    const int64_t tab_bytes = 3 * 4 * (int64_t)b.kch;
+    static const int cand[5][2] = {{4, 1}, {2, 2}, {2, 1}, {1, 2}, {1, 1}};
+    for (int pass = 0; pass < 2; ++pass) {
+        const int64_t lds_cap = pass == 0 ? kLdsBytes / 2 : kLdsBytes;
+        for (int i = 0; i < 5; ++i) {
+            const int cwm = cand[i][0], cwn = cand[i][1];
+            if (cwm == 4 && bits != 8)
+                continue;  // not instantiated: exceeds the register budget
+            const int MT = 32 * cwm;
+            if (MT > 32 && MT - 32 >= b.m)
+                continue;  // at least one full 32-channel row tile per extra tile row
+            if (MT > ((b.m + 31) / 32) * 32)
+                continue;
+            ConvArgs c = b;
+            int64_t lds = fit_tile(c, MT, 128 * cwn, bits, obits, (int64_t)MT * b.kp, tab_bytes, true);
+            if (lds < 0 || lds > lds_cap) {
+                c = b;
+                lds = fit_tile(c, MT, 128 * cwn, bits, obits, (int64_t)MT * b.kp, tab_bytes, true, true);
+            }
+            if (lds < 0 || lds > lds_cap)
+                continue;
+            const int64_t units = (int64_t)c.ntiles * ((c.m + MT - 1) / MT);
+            if (units < 2 * kPlanCus)
+                continue;
+            a = c;
+            wm = cwm;
+            wn = cwn;
+            return QNN_OK;
+        }
+    }
+    return QNN_ERR_UNSUPPORTED;
 }
 
 qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
@@ -323,10 +399,13 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.clip_lo = e->clip_lo;
     a.clip_hi = e->clip_hi;
     a.ypb = ypb;
-    int mr, nc, al16;
-    st = plan_conv_mfma(a, x->bits, mr, nc, al16);
-    if (st != QNN_OK)
-        return st;
+    int mr = 0, nc = 0, al16 = 0, wm = 0, wn = 0;
+    const bool use32 = plan_conv_m32(a, x->bits, wm, wn, al16) == QNN_OK;
+    if (!use32) {
+        st = plan_conv_mfma(a, x->bits, mr, nc, al16);
+        if (st != QNN_OK)
+            return st;
+    }
     a.quad16 = (pb % 16) == 0;
     a.pbq = (int32_t)(a.quad16 ? pb / 16 : pb / 4);
     a.div_pbq = make_fastdiv((uint32_t)a.pbq);
@@ -344,14 +423,15 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
         a.obq = 1;
     }
     a.div_obq = make_fastdiv((uint32_t)a.obq);
+    const int MT = use32 ? 32 * wm : 16 * mr;
     a.contig = a.epi == EPI_REQUANT && a.tw == a.wo && (a.ti == 1 || a.th == a.ho) &&
-               a.ot_b == ypb && (ypb % 4) == 0 && m <= 16 * mr;
+               a.ot_b == ypb && (ypb % 4) == 0 && m <= MT;
     a.div_qrow = make_fastdiv((uint32_t)(a.wrow / 16 > 0 ? a.wrow / 16 : 1));
-    a.div_ncol = make_fastdiv((uint32_t)(16 * a.ksteps));
+    // words per staged filter row: int8 chunks (16x16 kernel) or packed chunks
+    a.div_ncol = make_fastdiv((uint32_t)(use32 ? a.kch * x->bits / 2 : 4 * a.kch));
     st = device_info(&cus);
     if (st != QNN_OK)
         return st;
-    const int MT = 16 * mr;
     const int mtiles = (m + MT - 1) / MT;
     const int per_cu = a.lds_bytes * 2 <= kLdsBytes ? 2 : 1;
     int64_t gx = (int64_t)cus * per_cu;
@@ -361,12 +441,20 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
         gx = 1;
     dim3 grid((unsigned)gx, (unsigned)mtiles);
     hipError_t err;
-    if (x->bits == 8)
+    if (use32) {
+        if (x->bits == 8)
+            err = launch_conv_m32_b8(a, wm, wn, al16, grid, s);
+        else if (x->bits == 4)
+            err = launch_conv_m32_b4(a, wm, wn, al16, grid, s);
+        else
+            err = launch_conv_m32_b2(a, wm, wn, al16, grid, s);
+    } else if (x->bits == 8) {
         err = launch_conv_mfma_b8(a, mr, nc, al16, grid, s);
-    else if (x->bits == 4)
+    } else if (x->bits == 4) {
         err = launch_conv_mfma_b4(a, mr, nc, al16, grid, s);
-    else
+    } else {
         err = launch_conv_mfma_b2(a, mr, nc, al16, grid, s);
+    }
     return err == hipSuccess ? QNN_OK : QNN_ERR_LAUNCH;
 }
 

@@ -48,8 +48,11 @@ struct ConvArgs {
     // tiling of the output: tile = ti images x th rows x tw columns
     int32_t ti, th, tw, tiles_x, tiles_y, ntiles;
     int32_t hh, hwd, ps;   // halo rows / columns, local-memory pixel stride
-    int32_t kchunks, ksteps, kp;  // 16-byte K chunks, 64-deep MFMA steps, weight row stride
-    int32_t ot_b;          // output-tile bytes per pixel in local memory
+    int32_t kchunks, ksteps, kp;  // 16-byte K chunks, MFMA K steps, weight row stride in LDS
+    int32_t kch;           // chunks including the padding to whole K steps
+    int32_t ot_b;          // packed output bytes per pixel of a channel tile
+    int32_t cs;            // 32x32 kernel: bytes per pixel of the one-byte-per-code output staging
+    int32_t alias_out;     // 32x32 kernel: the output staging reuses the input tile's local memory
     int32_t off_tab, off_wsum, off_x, off_out, lds_bytes;
     int32_t row_mode, row_len, cpr;  // K walk per filter row when C*1B is not a multiple of 16
     FastDiv div_pbq;       // packed 16-byte (or 4-byte) quads per pixel
@@ -91,6 +94,9 @@ struct PoolArgs {
 hipError_t launch_conv_mfma_b8(const ConvArgs &a, int mr, int nc, int al16, dim3 grid, hipStream_t s);
 hipError_t launch_conv_mfma_b4(const ConvArgs &a, int mr, int nc, int al16, dim3 grid, hipStream_t s);
 hipError_t launch_conv_mfma_b2(const ConvArgs &a, int mr, int nc, int al16, dim3 grid, hipStream_t s);
+hipError_t launch_conv_m32_b8(const ConvArgs &a, int wm, int wn, int al16, dim3 grid, hipStream_t s);
+hipError_t launch_conv_m32_b4(const ConvArgs &a, int wm, int wn, int al16, dim3 grid, hipStream_t s);
+hipError_t launch_conv_m32_b2(const ConvArgs &a, int wm, int wn, int al16, dim3 grid, hipStream_t s);
 hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s);
 hipError_t launch_maxpool(const PoolArgs &a, int bits, hipStream_t s);
 hipError_t launch_relu_s8(const uint8_t *x, uint8_t *y, size_t count, hipStream_t s);
