@@ -97,9 +97,13 @@ __global__ void __launch_bounds__(256) conv_xnor_kernel(const uint32_t *__restri
 }
 
 // Register-resident variant (kd a multiple of 8): a lane gathers its whole
-// im2col column (kd <= KDM words, zero bits for padding taps) once, then loops over the output
-// channels; channel m's kd filter words are loaded by scalar loads and used
-// as scalar operands.  Only one channel's words are live at a time.
+// im2col column (kd <= KDM words, zero bits for padding taps) once, then
+// walks the output channels of its workgroup's channel group (grid.y; the
+// split keeps several waves per SIMD to hide the scalar-load latency).
+// Channel m's kd filter words arrive by scalar loads, 8 words ahead of their
+// use.  The lane counts mismatching bits, popcount(x ^ w): with K taps of
+// +-1 values, the dot product is K - 2 * mismatches, so no complement is
+// needed (two vector instructions per 32 binary MACs).
 template <int KDM>
 __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__restrict__ xg,
                                                             const uint32_t *__restrict__ wgl,
@@ -130,15 +134,23 @@ __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__re
         }
     }
 
+    const int mb = blockIdx.y * a.mgrp;
+    const int me = min(a.m, mb + a.mgrp);
+    int32_t b_cur = bias ? bias[mb] : 0;
+    int32_t t_cur = a.epi == EPI_RAW32 ? 0 : thresh[mb];
     uint32_t word = 0;
-    for (int m = 0; m < a.m; ++m) {
+    for (int m = mb; m < me; ++m) {
+        // the next channel's bias and threshold are fetched now, used next
+        const int mn = m + 1 < me ? m + 1 : m;
+        const int32_t b_next = bias ? bias[mn] : 0;
+        const int32_t t_next = a.epi == EPI_RAW32 ? 0 : thresh[mn];
         // kd is a multiple of 8: the filter row is walked in 32-byte blocks;
         // block b + 1 is fetched while block b is consumed, and the
         // scheduling barriers keep the compiler from hoisting every block's
         // scalar loads (which would spill scalar registers).
-        const uint4 *wr = (const uint4 *)(wgl + m * a.kd);
+        const uint4 *wr = (const uint4 *)(wgl + (size_t)m * a.kd);
         uint4 c0 = wr[0], c1 = wr[1];
-        uint32_t pop = 0;
+        uint32_t mis = 0;
 #pragma unroll
         for (int kb = 0; kb < KDM; kb += 8) {
             if (kb < a.kd) {
@@ -147,55 +159,61 @@ __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__re
                     n0 = wr[(kb + 8) / 4];
                     n1 = wr[(kb + 8) / 4 + 1];
                 }
-                pop += __popc(~(xv[kb + 0] ^ c0.x));
-                pop += __popc(~(xv[kb + 1] ^ c0.y));
-                pop += __popc(~(xv[kb + 2] ^ c0.z));
-                pop += __popc(~(xv[kb + 3] ^ c0.w));
-                pop += __popc(~(xv[kb + 4] ^ c1.x));
-                pop += __popc(~(xv[kb + 5] ^ c1.y));
-                pop += __popc(~(xv[kb + 6] ^ c1.z));
-                pop += __popc(~(xv[kb + 7] ^ c1.w));
+                mis += __popc(xv[kb + 0] ^ c0.x);
+                mis += __popc(xv[kb + 1] ^ c0.y);
+                mis += __popc(xv[kb + 2] ^ c0.z);
+                mis += __popc(xv[kb + 3] ^ c0.w);
+                mis += __popc(xv[kb + 4] ^ c1.x);
+                mis += __popc(xv[kb + 5] ^ c1.y);
+                mis += __popc(xv[kb + 6] ^ c1.z);
+                mis += __popc(xv[kb + 7] ^ c1.w);
                 c0 = n0;
                 c1 = n1;
             }
             __builtin_amdgcn_sched_barrier(0);
         }
-        const int64_t v = 2 * (int64_t)pop - a.kbits + (bias ? bias[m] : 0);
+        const int64_t v = (int64_t)a.kbits - 2 * (int64_t)mis + b_cur;
         if (a.epi == EPI_RAW32) {
             if (live)
                 ((int32_t *)a.y)[(size_t)p * a.m + m] = (int32_t)(uint32_t)(uint64_t)v;
-            continue;
-        }
-        word |= (v >= thresh[m] ? 1u : 0u) << (m & 31);
-        if ((m & 31) == 31 || m == a.m - 1) {
-            if (live) {
-                uint8_t *yb = a.y + (size_t)p * a.ypb + (m >> 5) * 4;
-                const int nb = min(4, a.ypb - (m >> 5) * 4);
-                if (nb == 4 && (a.ypb & 3) == 0) {
-                    *(uint32_t *)yb = word;
-                } else {
-                    for (int b = 0; b < nb; ++b)
-                        yb[b] = (uint8_t)(word >> (8 * b));
+        } else {
+            word |= (v >= t_cur ? 1u : 0u) << (m & 31);
+            if ((m & 31) == 31 || m == me - 1) {
+                if (live) {
+                    uint8_t *yb = a.y + (size_t)p * a.ypb + (m >> 5) * 4;
+                    const int nb = min(4, a.ypb - (m >> 5) * 4);
+                    if (nb == 4 && (a.ypb & 3) == 0) {
+                        *(uint32_t *)yb = word;
+                    } else {
+                        for (int b = 0; b < nb; ++b)
+                            yb[b] = (uint8_t)(word >> (8 * b));
+                    }
                 }
+                word = 0;
             }
-            word = 0;
         }
+        b_cur = b_next;
+        t_cur = t_next;
     }
 }
 
 hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s)
 {
     dim3 grid((a.npix + 255) / 256);
+    // channel groups of mgrp (a multiple of 32) along grid.y
+    dim3 grid_res(grid.x, (a.m + a.mgrp - 1) / a.mgrp);
     if (a.kd % 8 != 0 || a.kd > 128)
         ;
     else if (a.kd <= 32)
-        hipLaunchKernelGGL(conv_xnor_res_kernel<32>, grid, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
+        hipLaunchKernelGGL(conv_xnor_res_kernel<32>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
     else if (a.kd <= 64)
-        hipLaunchKernelGGL(conv_xnor_res_kernel<64>, grid, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
+        hipLaunchKernelGGL(conv_xnor_res_kernel<64>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
+    else if (a.kd <= 72)  // 3x3 taps of 256 channels
+        hipLaunchKernelGGL(conv_xnor_res_kernel<72>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
     else if (a.kd <= 96)
-        hipLaunchKernelGGL(conv_xnor_res_kernel<96>, grid, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
+        hipLaunchKernelGGL(conv_xnor_res_kernel<96>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
     else
-        hipLaunchKernelGGL(conv_xnor_res_kernel<128>, grid, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
+        hipLaunchKernelGGL(conv_xnor_res_kernel<128>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
     if (a.kd % 8 == 0 && a.kd <= 128)
         return hipGetLastError();
     if (a.cd % 8 == 0)

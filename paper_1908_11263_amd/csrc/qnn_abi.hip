@@ -376,6 +376,15 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
         a.epi = e->kind;
         a.ypb = ypb;
         a.npix = x->n * ho * wo;
+        {
+            // channel groups: enough waves per SIMD (about 4) to hide the
+            // latency of the scalar filter loads, groups of at least 32
+            const int64_t waves = ((int64_t)a.npix + 63) / 64;
+            int64_t groups = (4 * 4 * (int64_t)cus + waves - 1) / waves;
+            const int64_t maxg = (m + 31) / 32;
+            groups = groups < 1 ? 1 : (groups > maxg ? maxg : groups);
+            a.mgrp = (int32_t)((((m + groups - 1) / groups) + 31) / 32 * 32);
+        }
         a.div_wo = make_fastdiv((uint32_t)wo);
         a.div_ho = make_fastdiv((uint32_t)ho);
         a.div_cd = make_fastdiv((uint32_t)a.cd);

@@ -79,6 +79,7 @@ struct XnorArgs {
     int32_t m, kh, kw, sh, sw, ph, pw, ho, wo;
     int32_t kd, kbits, epi, ypb;
     int32_t npix;
+    int32_t mgrp;          // output channels per workgroup (multiple of 32), register-resident kernel
     FastDiv div_wo, div_ho, div_cd, div_kw;
 };
 
