@@ -28,7 +28,7 @@ PEAK_INT8_TOPS = 5000.0        # MI355X dense int8 matrix-core peak, 10^12 int o
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
 VALU_LANE_OPS = 256 * 64 * 2.4e9   # 32-bit vector lane-ops/s: 256 CUs x 64 lanes x 2.4 GHz
 XNOR_PEAK_BMACS = VALU_LANE_OPS * 16  # 2 lane-ops (xnor, bcnt) per 32 binary MACs
-PROFILE = os.path.join(ROOT, "profiles", "conv_mfma_int4_32x32x64_m64_b64_traffic.txt")
+PROFILE = os.path.join(ROOT, "profiles", "conv_int4_32x32x64_m64_b64_traffic.txt")
 
 
 def log(*a):
@@ -276,7 +276,7 @@ def main():
     traffic, kname = recorded_profile()
     roofline = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_INT8_TOPS,
                 "unit": "TOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 5),
-                "traffic": traffic, "kernel": kname or "conv_mfma_kernel (4-bit)",
+                "traffic": traffic, "kernel": kname or "conv_m32_kernel (4-bit)",
                 "ops_per_launch": 2 * head_step.macs}
     out = {
         "metric": "GMAC/s per qconv layer at INT8/4/2/1 (batch), % of int8 MFMA peak",
