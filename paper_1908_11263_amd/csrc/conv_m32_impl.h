@@ -139,16 +139,18 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     const bool wfast = !a.row_mode && (a.wrow & 15) == 0;
     const int qrow = a.wrow >> 4;
     const int nq = MT * qrow;
+    // quads of the rows that exist (rows past the last channel stay zero)
+    const int nqv = min(MT, a.m - m0) * qrow;
+    const uint4 *wsrc = (const uint4 *)(a.w + (size_t)m0 * a.wrow);
     constexpr int UW = 6;
     uint4 wq[UW];
     if (wfast) {
 #pragma unroll
         for (int u = 0; u < UW; ++u) {
             const int idx = tid + u * 256;
-            const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
             wq[u] = make_uint4(0, 0, 0, 0);
-            if (idx < nq && m0 + row < a.m)
-                wq[u] = *(const uint4 *)(a.w + (size_t)(m0 + row) * a.wrow + (idx - row * qrow) * 16);
+            if (idx < nqv)
+                wq[u] = wsrc[idx];
         }
     }
     int tile = blockIdx.x;
@@ -200,14 +202,14 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
         int hoff = 0, nat = 0, vld = 0;
         if (j < a.kchunks) {
             if (a.row_mode) {
-                int ky = j / a.cpr, r = (j - ky * a.cpr) * 16;
+                int ky = (int)fdiv((uint32_t)j, a.div_tab_a), r = (j - ky * a.cpr) * 16;
                 hoff = ky * a.hwd * a.ps + r;
                 nat = ky * a.row_len + r;
                 vld = min(16, a.row_len - r);
             } else {
                 int cpt = a.c8 >> 4;
-                int tap = j / cpt, c16 = j - tap * cpt;
-                int ky = tap / a.kw, kx = tap - ky * a.kw;
+                int tap = (int)fdiv((uint32_t)j, a.div_tab_a), c16 = j - tap * cpt;
+                int ky = (int)fdiv((uint32_t)tap, a.div_tab_kw), kx = tap - ky * a.kw;
                 hoff = (ky * a.hwd + kx) * a.ps + c16 * 16;
                 nat = j * 16;
                 vld = 16;
@@ -233,10 +235,9 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
 #pragma unroll
             for (int u = 0; u < UW; ++u) {
                 const int idx = b0 + u * 256;
-                const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
                 wq[u] = make_uint4(0, 0, 0, 0);
-                if (idx < nq && m0 + row < a.m)
-                    wq[u] = *(const uint4 *)(a.w + (size_t)(m0 + row) * a.wrow + (idx - row * qrow) * 16);
+                if (idx < nqv)
+                    wq[u] = wsrc[idx];
             }
 #pragma unroll
             for (int u = 0; u < UW; ++u) {
@@ -316,7 +317,10 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
 
     const int tile_px = a.ti * a.th * a.tw;
     const int h = lane >> 5, r32 = lane & 31;
-    const int cs = a.cs;
+    // code-staging pixel stride (the planner sizes sC with the same value):
+    // a compile-time stride turns every staging address into an immediate
+    // offset
+    constexpr int cs = MT + 16;
 
     for (bool first = true; tile < a.ntiles; tile += gridDim.x, first = false) {
         if (!first) {

@@ -335,14 +335,14 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
         int hoff = 0, nat = 0, vld = 0;
         if (j < a.kchunks) {
             if (a.row_mode) {
-                int ky = j / a.cpr, r = (j - ky * a.cpr) * 16;
+                int ky = (int)fdiv((uint32_t)j, a.div_tab_a), r = (j - ky * a.cpr) * 16;
                 hoff = ky * a.hwd * a.ps + r;
                 nat = ky * a.row_len + r;
                 vld = min(16, a.row_len - r);
             } else {
                 int cpt = a.c8 >> 4;
-                int tap = j / cpt, c16 = j - tap * cpt;
-                int ky = tap / a.kw, kx = tap - ky * a.kw;
+                int tap = (int)fdiv((uint32_t)j, a.div_tab_a), c16 = j - tap * cpt;
+                int ky = (int)fdiv((uint32_t)tap, a.div_tab_kw), kx = tap - ky * a.kw;
                 hoff = (ky * a.hwd + kx) * a.ps + c16 * 16;
                 nat = j * 16;
                 vld = 16;

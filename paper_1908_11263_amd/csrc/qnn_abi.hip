@@ -436,6 +436,8 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.contig = a.epi == EPI_REQUANT && a.tw == a.wo && (a.ti == 1 || a.th == a.ho) &&
                a.ot_b == ypb && (ypb % 4) == 0 && m <= MT;
     a.div_qrow = make_fastdiv((uint32_t)(a.wrow / 16 > 0 ? a.wrow / 16 : 1));
+    a.div_tab_a = make_fastdiv((uint32_t)(a.row_mode ? a.cpr : (a.c8 >> 4 > 0 ? a.c8 >> 4 : 1)));
+    a.div_tab_kw = make_fastdiv((uint32_t)a.kw);
     // words per staged filter row: int8 chunks (16x16 kernel) or packed chunks
     a.div_ncol = make_fastdiv((uint32_t)(use32 ? a.kch * x->bits / 2 : 4 * a.kch));
     st = device_info(&cus);

@@ -64,6 +64,8 @@ struct ConvArgs {
     FastDiv div_obq;       // output quads per pixel in the copy-out
     FastDiv div_qrow;      // packed 16-byte quads per filter bank
     FastDiv div_ncol;      // 4-byte words per staged filter row
+    FastDiv div_tab_a;     // K-chunk table: chunks per filter row (row walk) or per tap
+    FastDiv div_tab_kw;    // K-chunk table: filter columns
     int32_t pbq, quad16;   // quads per pixel, 1 if the quad is 16 bytes else 4 bytes
     int32_t ob0, obn, obq, oquad16;  // copy-out byte offset, byte count, quads, quad size flag
     int32_t contig;        // tile = consecutive output pixels with every channel: flat copy-out
