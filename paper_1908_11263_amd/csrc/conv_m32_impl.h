@@ -533,10 +533,21 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
                                                   : (size_t)T.n0 * a.ho * a.wo;
                 uint32_t *dst = (uint32_t *)(a.y + first_px * a.ypb);
                 const int nw = valid * a.obq;
-                for (int idx = tid; idx < nw; idx += 256) {
-                    const int p = (int)fdiv((uint32_t)idx, a.div_obq);
-                    const int q = idx - p * a.obq;
-                    dst[idx] = pack_codes_word<BITS>(sC + p * cs + q * CPW);
+                if ((a.obq & 3) == 0) {
+                    // four words (16 bytes) per store
+                    for (int i4 = tid * 4; i4 < nw; i4 += 256 * 4) {
+                        const int p = (int)fdiv((uint32_t)i4, a.div_obq);
+                        const uint8_t *src = sC + p * cs + (i4 - p * a.obq) * CPW;
+                        *(uint4 *)(dst + i4) = make_uint4(pack_codes_word<BITS>(src), pack_codes_word<BITS>(src + CPW),
+                                                          pack_codes_word<BITS>(src + 2 * CPW),
+                                                          pack_codes_word<BITS>(src + 3 * CPW));
+                    }
+                } else {
+                    for (int idx = tid; idx < nw; idx += 256) {
+                        const int p = (int)fdiv((uint32_t)idx, a.div_obq);
+                        const int q = idx - p * a.obq;
+                        dst[idx] = pack_codes_word<BITS>(sC + p * cs + q * CPW);
+                    }
                 }
             } else {
                 const int tq4 = tile_px * a.obq;
