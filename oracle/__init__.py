@@ -22,7 +22,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "qnn_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-REQUANT, THRESH1, RAW32 = 0, 1, 2
+REQUANT, THRESH1, RAW32, STAIR = 0, 1, 2, 3
 
 _lib = None
 
@@ -120,7 +120,7 @@ def conv2d(x, shape, bits, w, m, kh, kw, stride=(1, 1), pad=(0, 0), epi=RAW32, b
         if epi == RAW32:
             y = np.zeros((n, ho, wo, m), dtype=np.int32)
         else:
-            obits = bits if epi == REQUANT else 1
+            obits = bits if epi in (REQUANT, STAIR) else 1
             y = np.zeros((n, ho, wo, packed_bytes(m, obits)), dtype=np.uint8)
     rc = _load().oracle_conv2d(_ptr(x), n, h, wd, c, bits, _ptr(w), m, kh, kw, stride[0],
                                stride[1], pad[0], pad[1], epi, _ptr(b), _ptr(mu), _ptr(sh),
@@ -139,7 +139,7 @@ def linear(x, n, k, bits, w, m, epi=RAW32, bias=None, mult=None, shift=None, thr
     if epi == RAW32:
         y = np.zeros((n, m), dtype=np.int32)
     else:
-        y = np.zeros((n, packed_bytes(m, bits if epi == REQUANT else 1)), dtype=np.uint8)
+        y = np.zeros((n, packed_bytes(m, bits if epi in (REQUANT, STAIR) else 1)), dtype=np.uint8)
     rc = _load().oracle_linear(_ptr(x), n, k, bits, _ptr(w), m, epi, _ptr(b), _ptr(mu), _ptr(sh),
                                _ptr(th), clip[0], clip[1], _ptr(acc), _ptr(y))
     if rc != 0:

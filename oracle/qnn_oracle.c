@@ -38,6 +38,13 @@
  *   - requantization: y = clip(floor((acc + bias) * mult / 2^shift + 1/2));
  *     the product is taken without any overflow;
  *   - binary threshold: bit = (acc + bias >= thresh), acc the +1/-1 dot;
+ *   - staircase compression (Sec. III-A, Eq. (4)), 4 and 2 bits: each
+ *     channel has 2^Q - 1 thresholds tau_1 .. tau_{2^Q-1} and the output is
+ *     the level p of the interval [tau_p, tau_{p+1}) that holds acc + bias
+ *     (tau_0 = -inf, tau_{2^Q} = +inf).  For thresholds that are not
+ *     non-decreasing the intervals overlap or leave gaps; the library then
+ *     defines the output as the number of thresholds at or below acc + bias,
+ *     which is the same level whenever the thresholds are sorted;
  *   - RAW32 returns acc + bias reduced modulo 2^32 (two's complement).
  */
 #include <stdint.h>
@@ -46,7 +53,7 @@
 #include <stdlib.h>
 #include <pthread.h>
 
-enum { ORC_REQUANT = 0, ORC_THRESH1 = 1, ORC_RAW32 = 2 };
+enum { ORC_REQUANT = 0, ORC_THRESH1 = 1, ORC_RAW32 = 2, ORC_STAIR = 3 };
 
 /* Number of bytes that hold `count` codes of `bits` bits (whole bytes). */
 size_t oracle_packed_bytes(size_t count, int bits)
@@ -123,6 +130,34 @@ static __int128 floor_div_pow2(__int128 a, int s)
     return q;
 }
 
+/* Staircase compression of Sec. III-A, Eq. (4): Y = sum_p p * chi_[tau_p,
+ * tau_{p+1})(phi) over p = 0 .. 2^Q - 1 with tau_0 = -inf, tau_{2^Q} = +inf.
+ * `tau` holds tau_1 .. tau_{2^Q-1}.  With non-decreasing thresholds exactly
+ * one interval holds phi; otherwise the count of thresholds at or below phi
+ * is returned (the library's definition for unsorted thresholds). */
+static unsigned staircase(int64_t phi, const int32_t *tau, int q)
+{
+    const int levels = 1 << q;
+    int sorted = 1;
+    for (int p = 1; p + 1 < levels; ++p)
+        if (tau[p] < tau[p - 1])
+            sorted = 0;
+    if (sorted) {
+        for (int p = 0; p < levels; ++p) {
+            /* interval [tau_p, tau_{p+1}): lower end tau_p (p >= 1) */
+            int above_lower = p == 0 || phi >= (int64_t)tau[p - 1];
+            int below_upper = p == levels - 1 || phi < (int64_t)tau[p];
+            if (above_lower && below_upper)
+                return (unsigned)p;
+        }
+    }
+    unsigned count = 0;
+    for (int p = 1; p < levels; ++p)
+        if (phi >= (int64_t)tau[p - 1])
+            ++count;
+    return count;
+}
+
 /* INT-8 / sub-byte compression by scale and clamp (Sec. III-A). */
 static int64_t requant(int64_t v, int32_t mult, int shift, int32_t lo, int32_t hi)
 {
@@ -165,7 +200,7 @@ static void *conv_worker(void *arg)
     const conv_job *j = (const conv_job *)arg;
     const size_t xpix = oracle_packed_bytes((size_t)j->c, j->bits);
     const size_t wrow = oracle_packed_bytes((size_t)j->kh * j->kw * j->c, j->bits);
-    const int obits = j->epi == ORC_REQUANT ? j->bits : (j->epi == ORC_THRESH1 ? 1 : 32);
+    const int obits = (j->epi == ORC_REQUANT || j->epi == ORC_STAIR) ? j->bits : (j->epi == ORC_THRESH1 ? 1 : 32);
     const size_t ypix = obits == 32 ? (size_t)j->m * 4 : oracle_packed_bytes((size_t)j->m, obits);
     for (int32_t n = j->n0; n < j->n1; ++n)
         for (int32_t oy = 0; oy < j->ho; ++oy)
@@ -203,6 +238,9 @@ static void *conv_worker(void *arg)
                         put_code(yp, (size_t)mm, obits, (unsigned)q);
                     } else if (j->epi == ORC_THRESH1) {
                         put_code(yp, (size_t)mm, 1, (acc + b >= (int64_t)j->thresh[mm]) ? 1u : 0u);
+                    } else if (j->epi == ORC_STAIR) {
+                        const int nt = (1 << j->bits) - 1;
+                        put_code(yp, (size_t)mm, obits, staircase(acc + b, j->thresh + (size_t)mm * nt, j->bits));
                     } else {
                         uint32_t r = (uint32_t)(uint64_t)(acc + b); /* modulo 2^32 */
                         memcpy(yp + (size_t)mm * 4, &r, 4);
@@ -224,7 +262,8 @@ int32_t oracle_out_dim(int32_t in, int32_t k, int32_t stride, int32_t pad)
 /*
  * Quantized convolution.  Returns 0 on success, -1 on an argument the oracle
  * does not define.  `acc` (int64 [N][Ho][Wo][M]) and `y` are each optional.
- * y holds packed codes (REQUANT at the input bit-width, THRESH1 at 1 bit) or
+ * y holds packed codes (REQUANT and STAIR at the input bit-width, THRESH1
+ * at 1 bit; STAIR reads 2^bits - 1 thresholds per channel, channel-major) or
  * little-endian int32 values (RAW32), one output pixel after the other.
  */
 int oracle_conv2d(const uint8_t *x, int32_t n, int32_t h, int32_t w, int32_t c, int32_t bits,
@@ -242,6 +281,10 @@ int oracle_conv2d(const uint8_t *x, int32_t n, int32_t h, int32_t w, int32_t c, 
     if (epi == ORC_REQUANT && (bits == 1 || !mult || !shift))
         return -1;
     if (epi == ORC_THRESH1 && (bits != 1 || !thresh))
+        return -1;
+    if (epi == ORC_STAIR && ((bits != 4 && bits != 2) || !thresh))
+        return -1;
+    if (epi < ORC_REQUANT || epi > ORC_STAIR)
         return -1;
     int32_t ho = oracle_out_dim(h, kh, sh, ph), wo = oracle_out_dim(w, kw, sw, pw);
     if (ho < 1 || wo < 1)
@@ -284,8 +327,10 @@ int oracle_linear(const uint8_t *x, int32_t n, int32_t k, int32_t bits,
 {
     if (!(bits == 1 || bits == 2 || bits == 4 || bits == 8) || n < 0 || k < 1 || m < 1)
         return -1;
+    if (epi == ORC_STAIR && ((bits != 4 && bits != 2) || !thresh))
+        return -1;
     const size_t xrow = oracle_packed_bytes((size_t)k, bits);
-    const int obits = epi == ORC_REQUANT ? bits : (epi == ORC_THRESH1 ? 1 : 32);
+    const int obits = (epi == ORC_REQUANT || epi == ORC_STAIR) ? bits : (epi == ORC_THRESH1 ? 1 : 32);
     const size_t yrow = obits == 32 ? (size_t)m * 4 : oracle_packed_bytes((size_t)m, obits);
     for (int32_t nn = 0; nn < n; ++nn) {
         uint8_t *yp = y ? y + (size_t)nn * yrow : NULL;
@@ -305,6 +350,8 @@ int oracle_linear(const uint8_t *x, int32_t n, int32_t k, int32_t bits,
                 put_code(yp, (size_t)j, obits, (unsigned)requant(s + b, mult[j], shift[j], clip_lo, clip_hi));
             else if (epi == ORC_THRESH1)
                 put_code(yp, (size_t)j, 1, (s + b >= (int64_t)thresh[j]) ? 1u : 0u);
+            else if (epi == ORC_STAIR)
+                put_code(yp, (size_t)j, obits, staircase(s + b, thresh + (size_t)j * ((1 << bits) - 1), bits));
             else {
                 uint32_t r = (uint32_t)(uint64_t)(s + b);
                 memcpy(yp + (size_t)j * 4, &r, 4);

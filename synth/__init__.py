@@ -123,8 +123,11 @@ def _bits_draw(rng, size):
 
 def conv_layer(name, bits, n, h, w, c, m, k, pad, seed, x_rng, w_rng, bias_rng=None,
                mult_rng=(1 << 14, 1 << 15), shift=None, clip=None, thresh_rng=None, epi=None,
-               stride=1):
-    """Draw one layer's tensors in the fixed order x, w, bias, mult, thresh."""
+               stride=1, stair_sorted=True):
+    """Draw one layer's tensors in the fixed order x, w, bias, mult, thresh.
+
+    epi "stair" draws 2^bits - 1 thresholds per channel from thresh_rng,
+    sorted per channel unless stair_sorted is False."""
     rng = np.random.default_rng(seed)
     if bits == 1:
         x_vals = _bits_draw(rng, (n, h, w, c))
@@ -141,6 +144,10 @@ def conv_layer(name, bits, n, h, w, c, m, k, pad, seed, x_rng, w_rng, bias_rng=N
         shiftv = np.full(m, shift, dtype=np.int8)
     if bits == 1 and thresh_rng is not None:
         thresh = _draw(rng, thresh_rng[0], thresh_rng[1], m).astype(np.int32)
+    if epi == "stair":
+        thresh = _draw(rng, thresh_rng[0], thresh_rng[1], (m, (1 << bits) - 1)).astype(np.int32)
+        if stair_sorted:
+            thresh = np.sort(thresh, axis=1)
     return ConvLayer(name, bits, n, h, w, c, m, k, k, (stride, stride), (pad, pad), epi, x_vals,
                      w_vals, bias, mult, shiftv, thresh, clip or (0, 0))
 
@@ -271,6 +278,7 @@ def random_small_layer(rng, bits, epi=None):
                           stride=stride)
     hi = (1 << bits) - 1
     wlo, whi = -(1 << (bits - 1)), (1 << (bits - 1)) - 1
+    span = max(1, k * k * c * hi * whi // 4)  # thresholds of "stair" layers
     return conv_layer("rand_int%d" % bits, bits, n, h, w, c, m, k, pad, seed, (0, hi),
                       (wlo, whi), bias_rng=(-hi * 64, hi * 64), shift=int(rng.integers(8, 16)),
-                      clip=(0, hi), epi=epi, stride=stride)
+                      clip=(0, hi), epi=epi, stride=stride, thresh_rng=(-span, span))

@@ -8,7 +8,7 @@ import numpy as np
 
 import synth
 
-EPI = {"requant": 0, "thresh1": 1, "raw32": 2}
+EPI = {"requant": 0, "thresh1": 1, "raw32": 2, "stair": 3}
 
 
 def threads():

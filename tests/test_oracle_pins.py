@@ -9,6 +9,7 @@ Each test names what fixes the expected value:
     Sec. III-A Eq. (4) that scale-and-clamp must equal);
   * hand-worked values stored under tests/golden/ with their citation.
 """
+import bisect
 import os
 
 import numpy as np
@@ -21,7 +22,7 @@ import synth
 pytestmark = pytest.mark.filterwarnings("ignore::UserWarning")
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
-EPI = {"requant": 0, "thresh1": 1, "raw32": 2}
+EPI = {"requant": 0, "thresh1": 1, "raw32": 2, "stair": 3}
 
 
 def golden_lines(name):
@@ -173,7 +174,7 @@ def brute_force(L):
     wb = (L.kh * L.kw * L.c * L.bits + 7) // 8
     xs = L.x.reshape(L.n, L.h, L.w, pb)
     ws = L.wt.reshape(L.m, wb)
-    obits = {"requant": L.bits, "thresh1": 1, "raw32": 32}[L.epi]
+    obits = {"requant": L.bits, "thresh1": 1, "raw32": 32, "stair": L.bits}[L.epi]
     out = []
     for n in range(L.n):
         for oy in range(L.ho):
@@ -202,6 +203,9 @@ def brute_force(L):
                         code = min(max(r, L.clip[0]), L.clip[1])
                     elif L.epi == "thresh1":
                         code = 1 if v >= int(L.thresh[m]) else 0
+                    elif L.epi == "stair":
+                        # sorted thresholds: the level is how many lie at or below v
+                        code = bisect.bisect_right([int(t) for t in L.thresh[m]], v)
                     else:
                         code = v % (1 << 32)
                     word |= code << (m * obits)
@@ -222,7 +226,7 @@ def tiny_layers(bits, count, seed, epi):
 
 @pytest.mark.parametrize("bits,epi", [(8, "requant"), (4, "requant"), (2, "requant"),
                                       (8, "raw32"), (4, "raw32"), (2, "raw32"), (1, "raw32"),
-                                      (1, "thresh1")])
+                                      (1, "thresh1"), (4, "stair"), (2, "stair")])
 def test_oracle_matches_brute_force(orc, bits, epi):
     for L in tiny_layers(bits, 4, seed=200 + bits + len(epi), epi=epi):
         _, y = run_oracle(orc, L, want_acc=False)
@@ -340,6 +344,72 @@ def test_requant_equals_threshold_staircase(orc):
             taus = [-(-(p * (1 << (s + 1)) - (1 << s)) // (2 * M)) - b for p in range(1, hi + 1)]
             stair = (acc[:, None] >= np.array(taus)[None, :]).sum(axis=1)
             assert np.array_equal(y[:, j].astype(np.int64), stair), j
+
+
+def staircase_from_requant(bias, mult, shift, bits):
+    """Thresholds on acc (bias folded in) that reproduce scale-and-clamp with
+    clip (0, 2^bits - 1): level p is reached once (acc + b) mult + 2^(s-1) >=
+    p 2^s, i.e. acc >= ceil((p 2^s - 2^(s-1)) / mult) - b."""
+    m = len(bias)
+    nt = (1 << bits) - 1
+    tau = np.zeros((m, nt), dtype=np.int64)
+    for j in range(m):
+        s, M, b = int(shift[j]), int(mult[j]), int(bias[j])
+        half = (1 << (s - 1)) if s else 0
+        for p in range(1, nt + 1):
+            tau[j, p - 1] = -((half - p * (1 << s)) // M) - b
+    return tau
+
+
+@pytest.mark.parametrize("bits", [4, 2])
+def test_stair_equals_requant_with_derived_thresholds(orc, bits):
+    """The staircase epilogue (Eq. (4)) fed with the thresholds of a
+    multiplier/shift compression gives the same codes as scale-and-clamp."""
+    rng = np.random.default_rng(60 + bits)
+    hi = (1 << bits) - 1
+    count = 0
+    for L in tiny_layers(bits, 6, seed=70 + bits, epi="requant"):
+        L.clip = (0, hi)
+        _, want = run_oracle(orc, L, want_acc=False)
+        tau = staircase_from_requant(L.bias, L.mult, L.shift, bits)
+        if np.abs(tau).max() >= 1 << 31:
+            continue
+        _, got = orc.conv2d(L.x, (L.n, L.h, L.w, L.c), bits, L.wt, L.m, L.kh, L.kw, L.stride, L.pad,
+                            EPI["stair"], None, None, None, tau.astype(np.int32), (0, 0))
+        assert np.array_equal(got, want), L.name
+        count += 1
+    assert count >= 3
+    del rng
+
+
+@pytest.mark.parametrize("bits", [4, 2])
+def test_stair_unsorted_thresholds_count(orc, bits):
+    """Unsorted thresholds: the code is the number of thresholds at or below
+    acc + bias (checked by brute-force counting on the accumulators)."""
+    rng = np.random.default_rng(90 + bits)
+    L = synth.random_small_layer(rng, bits, epi="stair")
+    L.thresh = np.ascontiguousarray(rng.permuted(L.thresh, axis=1))
+    acc, y = run_oracle(orc, L)
+    b = L.bias.astype(np.int64)
+    phi = acc + b[None, None, None, :]
+    cnt = (phi[..., None] >= L.thresh.astype(np.int64)[None, None, None, :, :]).sum(axis=-1)
+    want = synth.pack_codes(cnt.reshape(-1, L.m), bits)
+    assert np.array_equal(y.reshape(want.shape), want)
+
+
+def test_hand_worked_stair(orc):
+    x1 = np.array([[1]], dtype=np.uint8)
+    for f in golden_lines("stair_examples.txt"):
+        bits, phi = int(f[0]), int(f[1])
+        tau = np.array([[int(t) for t in f[2].split(",")]], dtype=np.int32)
+        want = int(f[3])
+        # a 1-input linear layer with x = 1 and w = +1 (acc = 1, bias = phi - 1)
+        # or w = -1 (acc = -1, bias = phi + 1), whichever keeps the bias in int32
+        wcode = 1 if phi >= 0 else (1 << bits) - 1
+        bias = phi - 1 if phi >= 0 else phi + 1
+        _, y = orc.linear(x1, 1, 1, bits, np.array([[wcode]], dtype=np.uint8), 1, epi=EPI["stair"],
+                          bias=np.array([bias]), thresh=tau)
+        assert int(y[0, 0]) == want, f
 
 
 # ----------------------------------------------- P7 hand-worked examples
