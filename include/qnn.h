@@ -34,6 +34,13 @@
  *     shift[m] in [0, 62] (out-of-range shifts give unspecified codes; they
  *     never fault).
  *   QNN_EPI_THRESH1 (b = 1; output 1 bit): y = (acc + bias[m] >= thresh[m]).
+ *   QNN_EPI_STAIR (b = 4, 2; output b bits; Sec. III-A, Eq. (4)): thresh
+ *     holds T = 2^b - 1 thresholds per channel, channel-major
+ *     (thresh[m*T + p - 1] = tau_p); y is the level p of the interval
+ *     [tau_p, tau_{p+1}) that holds acc + bias[m] (tau_0 = -inf,
+ *     tau_{2^b} = +inf), compared exactly in 64 bits.  For thresholds that
+ *     are not non-decreasing, y is the number of thresholds at or below
+ *     acc + bias[m] (the same level whenever they are sorted).
  *   QNN_EPI_RAW32 (any b; output int32 per channel): y = acc + bias[m],
  *     reduced modulo 2^32.
  *   bias may be NULL (zero).
@@ -62,7 +69,7 @@
 extern "C" {
 #endif
 
-#define QNN_ABI_VERSION 1
+#define QNN_ABI_VERSION 2
 
 typedef enum {
     QNN_OK = 0,
@@ -80,7 +87,8 @@ typedef enum {
 typedef enum {
     QNN_EPI_REQUANT = 0,
     QNN_EPI_THRESH1 = 1,
-    QNN_EPI_RAW32 = 2
+    QNN_EPI_RAW32 = 2,
+    QNN_EPI_STAIR = 3
 } qnn_epilogue;
 
 /* An NHWC tensor: n images of h x w pixels with c channels of `bits` bits
@@ -100,7 +108,7 @@ typedef struct {
     const int32_t *bias;     /* [M] or NULL */
     const int32_t *mult;     /* [M], QNN_EPI_REQUANT */
     const int8_t *shift;     /* [M], QNN_EPI_REQUANT, each in [0, 62] */
-    const int32_t *thresh;   /* [M], QNN_EPI_THRESH1 */
+    const int32_t *thresh;   /* [M] (QNN_EPI_THRESH1) or [M][2^b - 1] (QNN_EPI_STAIR) */
     int32_t clip_lo, clip_hi;/* QNN_EPI_REQUANT output range */
 } qnn_epi;
 
@@ -131,8 +139,8 @@ qnn_status qnn_conv2d_out_shape(const qnn_tensor *x, int32_t m, const qnn_conv_g
  *   x, x_dev: input descriptor and packed NHWC device data (bits 8, 4, 2, 1).
  *   m, w_dev: number of filters and packed M x kh x kw x C weights at the
  *             same bit-width as the input.
- *   g:        geometry; e: epilogue (REQUANT at 8/4/2 bits, THRESH1 at 1 bit,
- *             RAW32 at any).
+ *   g:        geometry; e: epilogue (REQUANT at 8/4/2 bits, STAIR at 4/2 bits,
+ *             THRESH1 at 1 bit, RAW32 at any).
  *   y, y_dev: output descriptor (must equal qnn_conv2d_out_shape) and device
  *             buffer of qnn_tensor_bytes(y) bytes; must not overlap the inputs.
  */

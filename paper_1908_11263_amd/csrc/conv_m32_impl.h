@@ -118,7 +118,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     int32_t *sNat = sTab + kch;
     int32_t *sVld = sNat + kch;
     int32_t *sWsum = (int32_t *)(smem + a.off_wsum);            // [MT] filter sums, [4] votes
-    int4 *sEpi = (int4 *)(smem + a.off_wsum + 4 * MT + 16);      // [MT][2] requantization plans
+    int4 *sEpi = (int4 *)(smem + a.off_wsum + 4 * MT + 16);      // [MT][4]: plan (2) or 16 thresholds
     uint8_t *sX = smem + a.off_x;
     uint8_t *sC = smem + a.off_out;                              // [pixel][cs] one byte per code
 
@@ -168,9 +168,15 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     // are computed while the loads above are in flight) and the votes that
     // select a workgroup-uniform epilogue
     constexpr int SL = BITS == 4 ? 4 : (BITS == 2 ? 6 : 0);
+    constexpr int NT = BITS == 8 ? 1 : (1 << BITS) - 1;  // staircase thresholds per channel
     auto make_plans = [&](const int32_t *wsum) {
         int mode = 0;
-        if (has_ch) {
+        if (has_ch && a.epi == EPI_STAIR) {
+            const bool live = m0 + pch < a.m;
+            stair_thresholds(live ? a.thresh + (size_t)(m0 + pch) * NT : nullptr, NT, p_bias, SL,
+                             (int32_t *)(sEpi + 4 * pch));
+            mode = 5;
+        } else if (has_ch) {
             int4 e0, e1;
             if (m0 + pch < a.m) {
                 int64_t b = p_bias;
@@ -182,8 +188,8 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
                 e0 = make_int4(0, 0, 0, 0);
                 e1 = make_int4(0, 0, 3, 0);
             }
-            sEpi[2 * pch] = e0;
-            sEpi[2 * pch + 1] = e1;
+            sEpi[4 * pch] = e0;
+            sEpi[4 * pch + 1] = e1;
             mode = e1.z;
         }
         const bool v3 = __all(!has_ch || mode == 3);
@@ -432,7 +438,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
 #pragma unroll
             for (int t = 0; t < WM; ++t) {
                 const int mg = m0 + t * 32 + r32;
-                const int4 e0 = sEpi[2 * (t * 32 + r32)];
+                const int4 e0 = sEpi[4 * (t * 32 + r32)];
                 const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);
 #pragma unroll
                 for (int c = 0; c < WN; ++c)
@@ -463,8 +469,28 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
 #pragma unroll
             for (int t = 0; t < WM; ++t) {
                 const int ch = t * 32 + r32;
-                const int4 e0 = sEpi[2 * ch];
-                const int4 e1 = sEpi[2 * ch + 1];
+                if (BITS != 8 && a.epi == EPI_STAIR) {
+                    // staircase (Eq. (4)): count the channel's thresholds at or below acc'
+                    int32_t T[16];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const int4 q4 = sEpi[4 * ch + k];
+                        T[4 * k] = q4.x;
+                        T[4 * k + 1] = q4.y;
+                        T[4 * k + 2] = q4.z;
+                        T[4 * k + 3] = q4.w;
+                    }
+#pragma unroll
+                    for (int c = 0; c < WN; ++c) {
+                        uint8_t *dst = sC + (wv * 32 * WN + c * 32 + 4 * h) * cs + ch;
+#pragma unroll
+                        for (int v = 0; v < 16; ++v)
+                            dst[(8 * (v >> 2) + (v & 3)) * cs] = (uint8_t)stair_level<NT>((int32_t)acc[t][c][v], T);
+                    }
+                    continue;
+                }
+                const int4 e0 = sEpi[4 * ch];
+                const int4 e1 = sEpi[4 * ch + 1];
 #pragma unroll
                 for (int c = 0; c < WN; ++c) {
                     uint8_t *dst = sC + (wv * 32 * WN + c * 32 + 4 * h) * cs + ch;

@@ -180,6 +180,39 @@ __device__ __forceinline__ void requant_plan(int64_t bias, int32_t mult, int32_t
     e1 = make_int4((int32_t)Q, shift, R + D * (int64_t)mult < ((int64_t)1 << 32) ? 1 : 2, 0);
 }
 
+// Staircase thresholds of one channel (Sec. III-A, Eq. (4)) moved onto the
+// kernel's accumulator: acc + bias >= tau  <=>  S acc >= S (tau - bias), with
+// S = 2^scale_log2 the weight scale of the sub-byte staging.  Values are
+// clamped to int32: S acc never equals INT32_MAX (an odd number, S acc is a
+// multiple of S), so the clamped comparisons keep their results.  Unused
+// slots (and missing channels) hold INT32_MAX, which no accumulator reaches.
+__device__ __forceinline__ void stair_thresholds(const int32_t *tau, int nt, int64_t bias,
+                                                 int scale_log2, int32_t *dst16)
+{
+#pragma unroll
+    for (int p = 0; p < 16; ++p) {
+        int32_t v = INT32_MAX;
+        if (tau && p < nt) {
+            int64_t t = ((int64_t)tau[p] - bias) * ((int64_t)1 << scale_log2);
+            t = t < INT32_MIN ? INT32_MIN : (t > INT32_MAX ? INT32_MAX : t);
+            v = (int32_t)t;
+        }
+        dst16[p] = v;
+    }
+}
+
+// Staircase level of a (scaled) accumulator: the number of thresholds at or
+// below it.
+template <int NT>
+__device__ __forceinline__ uint32_t stair_level(int32_t acc, const int32_t *T)
+{
+    uint32_t code = 0;
+#pragma unroll
+    for (int p = 0; p < NT; ++p)
+        code += acc >= T[p] ? 1u : 0u;
+    return code;
+}
+
 // One batch of U packed-input quads of a tile: issue the loads ...
 template <int BITS, bool Q16, int U>
 __device__ __forceinline__ void halo_issue(const ConvArgs &a, int b0, int totq, int n0, int iy0,
@@ -281,7 +314,7 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
     int32_t *sNat = sTab + kch;
     int32_t *sVld = sNat + kch;
     int32_t *sWsum = (int32_t *)(smem + a.off_wsum);           // [MT] filter sums (8 bits), [4] votes
-    int4 *sEpi = (int4 *)(smem + a.off_wsum + 4 * MT + 16);      // [MT][2] requantization plans
+    int4 *sEpi = (int4 *)(smem + a.off_wsum + 4 * MT + 16);      // [MT][4]: plan (2) or 16 thresholds
     uint8_t *sX = smem + a.off_x;
     uint8_t *sOut = smem + a.off_out;
 
@@ -459,8 +492,14 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
         __syncthreads();
     }
     constexpr int SL = BITS == 4 ? 4 : (BITS == 2 ? 6 : 0);  // log2 of the weight scale
+    constexpr int NT = BITS == 8 ? 1 : (1 << BITS) - 1;       // staircase thresholds per channel
     int mode = 0;
-    if (has_ch) {
+    if (has_ch && a.epi == EPI_STAIR) {
+        const bool live = m0 + pch < a.m;
+        stair_thresholds(live ? a.thresh + (size_t)(m0 + pch) * NT : nullptr, NT, p_bias, SL,
+                         (int32_t *)(sEpi + 4 * pch));
+        mode = 5;
+    } else if (has_ch) {
         int4 e0, e1;
         if (m0 + pch < a.m) {
             int64_t b = p_bias;
@@ -473,8 +512,8 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
             e0 = make_int4(0, 0, 0, 0);
             e1 = make_int4(0, 0, 3, 0);
         }
-        sEpi[2 * pch] = e0;
-        sEpi[2 * pch + 1] = e1;
+        sEpi[4 * pch] = e0;
+        sEpi[4 * pch + 1] = e1;
         mode = e1.z;
     }
     // workgroup-uniform epilogue selection: per-wave votes in LDS, then the
@@ -498,16 +537,15 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
     const int tile_px = a.ti * a.th * a.tw;
     const int g = lane >> 4, r16 = lane & 15;
 
-    for (; tile < a.ntiles; tile += gridDim.x) {
-        // the next tile's first input batch is loaded into registers now and
-        // lands in LDS after this tile's MFMAs and epilogue, so its latency
-        // hides behind them
-        const int next = tile + gridDim.x;
-        TileXY Tn = tile_xy(a, next < a.ntiles ? next : tile);
-        if (a.quad16)
-            halo_issue<BITS, true, UH>(a, tid, next < a.ntiles ? totq : 0, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
-        else
-            halo_issue<BITS, false, UH>(a, tid, next < a.ntiles ? totq : 0, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
+    for (bool first = true; tile < a.ntiles; tile += gridDim.x, first = false) {
+        if (!first) {
+            T = tile_xy(a, tile);
+            if (a.quad16)
+                halo_stage_from<BITS, true, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
+            else
+                halo_stage_from<BITS, false, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
+            __syncthreads();
+        }
 
         // ---- main loop: MR x NC MFMA tiles per 64-deep K step ----
         int base[NC];
@@ -598,7 +636,7 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                     const int mrow = t * 16 + 4 * g + i + ez;
                     if (m0 + mrow >= a.m)
                         continue;
-                    const int4 e0 = ep[2 * mrow];
+                    const int4 e0 = ep[4 * mrow];
                     const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);
 #pragma unroll
                     for (int c = 0; c < NC; ++c) {
@@ -619,15 +657,35 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
                     packed[t][c] = 0;
-            if (all3 || all4) {
+            if (BITS != 8 && a.epi == EPI_STAIR) {
+                // staircase (Eq. (4)): count the channel's thresholds at or below acc'
+#pragma unroll
+                for (int t = 0; t < MR; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int4 *tp = ep + 4 * (t * 16 + 4 * g + i + ez);
+                        int32_t T[16];
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            const int4 q4 = tp[k];
+                            T[4 * k] = q4.x;
+                            T[4 * k + 1] = q4.y;
+                            T[4 * k + 2] = q4.z;
+                            T[4 * k + 3] = q4.w;
+                        }
+#pragma unroll
+                        for (int c = 0; c < NC; ++c)
+                            packed[t][c] |= stair_level<NT>((int32_t)acc[t][c][i], T) << (i * BITS);
+                    }
+            } else if (all3 || all4) {
                 // strict plan: code = (clamp(acc' - A, 0, DS) * mult + RS) >> shift'
 #pragma unroll
                 for (int t = 0; t < MR; ++t) {
                     int4 e0[4], e1[4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        e0[i] = ep[2 * (t * 16 + 4 * g + i + ez)];
-                        e1[i] = ep[2 * (t * 16 + 4 * g + i + ez) + 1];
+                        e0[i] = ep[4 * (t * 16 + 4 * g + i + ez)];
+                        e1[i] = ep[4 * (t * 16 + 4 * g + i + ez) + 1];
                     }
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
@@ -654,8 +712,8 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                     int4 e0[4], e1[4];
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
-                        e0[i] = ep[2 * (t * 16 + 4 * g + i + ez)];
-                        e1[i] = ep[2 * (t * 16 + 4 * g + i + ez) + 1];
+                        e0[i] = ep[4 * (t * 16 + 4 * g + i + ez)];
+                        e1[i] = ep[4 * (t * 16 + 4 * g + i + ez) + 1];
                     }
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
@@ -693,8 +751,8 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                         const int mrow = t * 16 + 4 * g + i + ez;
                         if (m0 + mrow >= a.m)
                             continue;
-                        const int4 e0 = ep[2 * mrow];
-                        const int4 e1 = ep[2 * mrow + 1];
+                        const int4 e0 = ep[4 * mrow];
+                        const int4 e1 = ep[4 * mrow + 1];
 #pragma unroll
                         for (int c = 0; c < NC; ++c) {
                             if (e1.z >= 3) {
@@ -784,20 +842,8 @@ __global__ void __launch_bounds__(256, 2) conv_mfma_kernel(ConvArgs a)
                 }
             }
         }
-        // every wave is past this tile's MFMAs (barrier above): the next input
-        // tile may overwrite sX; the barrier below also keeps the next
-        // epilogue from overwriting sOut before this copy-out is done
-        if (next < a.ntiles) {
-            if (a.quad16) {
-                halo_store<BITS, true, UH>(sX, hq, hd);
-                halo_stage_from<BITS, true, UH>(a, sX, tid + 256 * UH, Tn.n0, Tn.iy0, Tn.ix0);
-            } else {
-                halo_store<BITS, false, UH>(sX, hq, hd);
-                halo_stage_from<BITS, false, UH>(a, sX, tid + 256 * UH, Tn.n0, Tn.iy0, Tn.ix0);
-            }
-        }
-        T = Tn;
-        __syncthreads();
+        // the next tile's input staging overwrites sX / sOut only after every
+        // wave passed the barrier above; its own barrier follows the staging
     }
 }
 

@@ -66,7 +66,7 @@ int32_t out_dim(int32_t in, int32_t k, int32_t s, int32_t p)
 
 int out_bits_for(int32_t kind, int32_t in_bits)
 {
-    if (kind == QNN_EPI_REQUANT)
+    if (kind == QNN_EPI_REQUANT || kind == QNN_EPI_STAIR)
         return in_bits;
     if (kind == QNN_EPI_THRESH1)
         return 1;
@@ -108,6 +108,12 @@ qnn_status check_epi(const qnn_epi *e, int bits, int32_t m)
         break;
     case QNN_EPI_THRESH1:
         if (bits != 1)
+            return QNN_ERR_BITS;
+        if (!e->thresh)
+            return QNN_ERR_NULL;
+        break;
+    case QNN_EPI_STAIR:
+        if (bits != 4 && bits != 2)
             return QNN_ERR_BITS;
         if (!e->thresh)
             return QNN_ERR_NULL;
@@ -154,7 +160,7 @@ int64_t fit_tile(ConvArgs &c, int MT, int PT, int bits, int obits, int64_t w_byt
     off += tab_bytes;
     off = (off + 15) & ~(int64_t)15;
     const int64_t off_wsum = off;
-    off += 4 * MT + 16 + 32 * MT;   // filter sums, votes, requantization plans
+    off += 4 * MT + 16 + 64 * MT;   // filter sums, votes, per-channel plans or staircase thresholds
     off = (off + 15) & ~(int64_t)15;
     const int64_t off_x = off;
     off += (x_bytes + 15) & ~(int64_t)15;
@@ -224,7 +230,7 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
     a.ksteps = (a.kchunks + 3) / 4;
     a.kch = 4 * a.ksteps;
     a.kp = a.ksteps * 64 + 16;
-    const int obits = a.epi == EPI_REQUANT ? bits : 32;
+    const int obits = a.epi == EPI_RAW32 ? 32 : bits;
     const int64_t tab_bytes = 3 * 4 * (int64_t)a.kch;
     const int mr_first = a.m <= 16 ? 1 : (a.m <= 32 ? 2 : 4);
     ConvArgs best = a;
@@ -277,7 +283,7 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16)
     b.kch = 2 * b.ksteps;
     const int cb = 2 * bits;         // packed bytes per 16-byte K chunk
     b.kp = (b.kch + 1) * cb;         // odd multiple of cb: conflict-free fragment reads
-    const int obits = b.epi == EPI_REQUANT ? bits : 32;
+    const int obits = b.epi == EPI_RAW32 ? 32 : bits;
     const int64_t tab_bytes = 3 * 4 * (int64_t)b.kch;
     static const int cand[5][2] = {{4, 1}, {2, 2}, {2, 1}, {1, 2}, {1, 1}};
     for (int pass = 0; pass < 2; ++pass) {
@@ -400,6 +406,7 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.bias = e->bias;
     a.mult = e->mult;
     a.shift = e->shift;
+    a.thresh = e->thresh;
     a.n = x->n; a.h = x->h; a.w_ = x->w; a.pb = (int32_t)pb; a.c8 = x->c;
     a.m = m; a.kh = g->kh; a.kw = g->kw; a.sh = g->stride_h; a.sw = g->stride_w;
     a.ph = g->pad_h; a.pw = g->pad_w; a.ho = ho; a.wo = wo;
@@ -424,7 +431,7 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.div_tw = make_fastdiv((uint32_t)a.tw);
     a.div_tx = make_fastdiv((uint32_t)a.tiles_x);
     a.div_ty = make_fastdiv((uint32_t)a.tiles_y);
-    if (a.epi == EPI_REQUANT) {
+    if (a.epi != EPI_RAW32) {
         a.oquad16 = (ypb % 4) == 0;   // copy whole 4-byte words when every tile's range is word-sized
         a.obq = a.oquad16 ? a.ot_b / 4 : a.ot_b;
     } else {
@@ -433,7 +440,7 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     }
     a.div_obq = make_fastdiv((uint32_t)a.obq);
     const int MT = use32 ? 32 * wm : 16 * mr;
-    a.contig = a.epi == EPI_REQUANT && a.tw == a.wo && (a.ti == 1 || a.th == a.ho) &&
+    a.contig = a.epi != EPI_RAW32 && a.tw == a.wo && (a.ti == 1 || a.th == a.ho) &&
                a.ot_b == ypb && (ypb % 4) == 0 && m <= MT;
     a.div_qrow = make_fastdiv((uint32_t)(a.wrow / 16 > 0 ? a.wrow / 16 : 1));
     a.div_tab_a = make_fastdiv((uint32_t)(a.row_mode ? a.cpr : (a.c8 >> 4 > 0 ? a.c8 >> 4 : 1)));
@@ -519,9 +526,11 @@ qnn_status qnn_conv2d_out_shape(const qnn_tensor *x, int32_t m, const qnn_conv_g
         return QNN_ERR_SHAPE;
     if (g->kh < 1 || g->kw < 1 || g->stride_h < 1 || g->stride_w < 1 || g->pad_h < 0 || g->pad_w < 0)
         return QNN_ERR_PARAM;
-    if (kind != QNN_EPI_REQUANT && kind != QNN_EPI_THRESH1 && kind != QNN_EPI_RAW32)
+    if (kind != QNN_EPI_REQUANT && kind != QNN_EPI_THRESH1 && kind != QNN_EPI_RAW32 &&
+        kind != QNN_EPI_STAIR)
         return QNN_ERR_PARAM;
-    if ((kind == QNN_EPI_REQUANT && x->bits == 1) || (kind == QNN_EPI_THRESH1 && x->bits != 1))
+    if ((kind == QNN_EPI_REQUANT && x->bits == 1) || (kind == QNN_EPI_THRESH1 && x->bits != 1) ||
+        (kind == QNN_EPI_STAIR && x->bits != 4 && x->bits != 2))
         return QNN_ERR_BITS;
     const int32_t ho = out_dim(x->h, g->kh, g->stride_h, g->pad_h);
     const int32_t wo = out_dim(x->w, g->kw, g->stride_w, g->pad_w);

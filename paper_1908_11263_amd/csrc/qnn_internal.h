@@ -29,7 +29,7 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv &f)
     return (__umulhi(n, f.mul) + n) >> f.shr;
 }
 
-enum { EPI_REQUANT = 0, EPI_THRESH1 = 1, EPI_RAW32 = 2 };
+enum { EPI_REQUANT = 0, EPI_THRESH1 = 1, EPI_RAW32 = 2, EPI_STAIR = 3 };
 
 // Arguments of the int8-MFMA implicit-GEMM convolution (8/4/2-bit inputs).
 // GEMM view: rows = output channels (A = weights), columns = output pixels
@@ -40,6 +40,7 @@ struct ConvArgs {
     uint8_t *y;            // packed NHWC output (codes) or int32 [pix][M]
     const int32_t *bias, *mult;
     const int8_t *shift;
+    const int32_t *thresh; // staircase thresholds [M][2^bits - 1]
     int32_t n, h, w_, pb;  // input size, packed bytes per pixel
     int32_t c8;            // channels (= bytes of an unpacked int8 pixel)
     int32_t m, kh, kw, sh, sw, ph, pw, ho, wo;

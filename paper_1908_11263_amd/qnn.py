@@ -17,8 +17,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqnn.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "qnn.h")
 
-EPI_REQUANT, EPI_THRESH1, EPI_RAW32 = 0, 1, 2
-_EPI_NAMES = {"requant": EPI_REQUANT, "thresh1": EPI_THRESH1, "raw32": EPI_RAW32}
+EPI_REQUANT, EPI_THRESH1, EPI_RAW32, EPI_STAIR = 0, 1, 2, 3
+_EPI_NAMES = {"requant": EPI_REQUANT, "thresh1": EPI_THRESH1, "raw32": EPI_RAW32, "stair": EPI_STAIR}
 
 STATUS = {
     0: "QNN_OK", 1: "QNN_ERR_NULL", 2: "QNN_ERR_BITS", 3: "QNN_ERR_SHAPE", 4: "QNN_ERR_PARAM",

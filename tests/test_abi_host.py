@@ -25,7 +25,7 @@ def test_exports_every_header_function(q, L):
     assert len(names) >= 12
     for name in names:
         assert hasattr(L, name), name
-    assert L.qnn_abi_version() == 1
+    assert L.qnn_abi_version() == 2
 
 
 def test_status_strings(q, L):
@@ -100,6 +100,24 @@ def test_int1_requires_threshold_or_raw(q, L):
                      (1, 4, 4, 8, 1)) == 2
     assert call_conv(q, L, (1, 4, 4, 32), 1, 8, (3, 3, 1, 1, 1, 1), (1, None, None, None, None, 0, 0),
                      (1, 4, 4, 8, 1)) == 1
+
+
+def test_stair_validation(q, L):
+    """The staircase epilogue is defined at 4 and 2 bits and needs thresholds."""
+    g = (3, 3, 1, 1, 1, 1)
+    st4 = (3, None, None, None, FAKE, 0, 0)
+    assert q.out_shape((1, 4, 4, 64), 4, 16, 3, 3, (1, 1), (1, 1), "stair") == (1, 4, 4, 16, 4)
+    assert q.out_shape((1, 4, 4, 128), 2, 16, 3, 3, (1, 1), (1, 1), "stair") == (1, 4, 4, 16, 2)
+    for bits, c in ((8, 32), (1, 32)):
+        with pytest.raises(q.QnnError) as e:
+            q.out_shape((1, 4, 4, c), bits, 16, 3, 3, (1, 1), (1, 1), "stair")
+        assert e.value.status == 2
+    assert call_conv(q, L, (1, 4, 4, 32), 8, 16, g, st4, (1, 4, 4, 16, 8)) == 2
+    assert call_conv(q, L, (1, 4, 4, 64), 4, 16, g, (3, None, None, None, None, 0, 0),
+                     (1, 4, 4, 16, 4)) == 1
+    # a valid call gets past every host check (no GPU here: device error)
+    assert call_conv(q, L, (1, 4, 4, 64), 4, 16, g, st4, (1, 4, 4, 16, 4)) == 8
+    assert call_conv(q, L, (1, 4, 4, 128), 2, 16, g, st4, (1, 4, 4, 16, 2)) == 8
 
 
 def test_unsupported_local_memory(q, L):
