@@ -237,6 +237,7 @@ def main():
         "int4": lambda: ConvStep(synth.int4_layer()),
         "int2": lambda: ConvStep(synth.int2_layer()),
         "int1": lambda: ConvStep(synth.int1_layer()),
+        "int4_stair": lambda: ConvStep(synth.int4_stair_layer()),
         "cifar8": lambda: NetworkStep(synth.cifar_network(8, n=4096)),
         "cifar4": lambda: NetworkStep(synth.cifar_network(4, n=4096)),
     }

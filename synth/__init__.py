@@ -169,6 +169,15 @@ def int4_layer(n=64):
                       clip=(0, 15))
 
 
+def int4_stair_layer(n=64):
+    """The INT4 layer's shape and seed with the staircase epilogue of
+    Sec. III-A, Eq. (4): 15 sorted thresholds per channel drawn from
+    U[-15120, 15120] (a quarter of K * max x * max w)."""
+    return conv_layer("int4_stair_32x32x64_m64_b%d" % n, 4, n, 32, 32, 64, 64, 3, 1, seed=1,
+                      x_rng=(0, 15), w_rng=(-8, 7), bias_rng=(-256, 256),
+                      thresh_rng=(-15120, 15120), epi="stair")
+
+
 def int2_layer(n=256):
     """INT2 3x3 layer, 16x16x128 input, 128 filters."""
     return conv_layer("int2_16x16x128_m128_b%d" % n, 2, n, 16, 16, 128, 128, 3, 1, seed=2,

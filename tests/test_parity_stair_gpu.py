@@ -115,3 +115,11 @@ def test_stair_extreme_thresholds(qnn, orc):
             L.bias = np.where(np.arange(m) % 2 == 0, (1 << 31) - 1, -(1 << 31)).astype(np.int32)
             check(orc, L)
             del nt
+
+
+def test_stair_bench_workload(qnn, orc):
+    """The benchmarked staircase layer (INT4, batch 64, 32x32x64 -> 64)."""
+    L = synth.int4_stair_layer()
+    y = check(orc, L, images=sample_images(L.n, k=4, seed=11))
+    codes = np.concatenate([(y & 15).ravel(), (y >> 4).ravel()])
+    log("int4 stair codes: min %d max %d distinct %d" % (codes.min(), codes.max(), len(np.unique(codes))))
