@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define QNN_ABI_VERSION 2
+#define QNN_ABI_VERSION 3
 
 typedef enum {
     QNN_OK = 0,
@@ -157,6 +157,23 @@ qnn_status qnn_conv2d(const qnn_tensor *x, const void *x_dev, int32_t m, const v
  */
 qnn_status qnn_linear(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
                       const qnn_epi *e, const qnn_tensor *y, void *y_dev, void *stream);
+
+/*
+ * Convolution fused with the 2x2 / stride-2 max-pooling that follows it in
+ * the paper's network (Sec. IV-A pooling kernel): y = maxpool_2x2/2 of the
+ * codes qnn_conv2d would produce, floor output size, in one pass (the
+ * convolution's output never reaches memory).
+ *   e:      QNN_EPI_REQUANT (8/4/2 bits) or QNN_EPI_STAIR (4/2 bits); other
+ *           epilogues give QNN_ERR_PARAM.
+ *   pool_k, pool_s: pooling window and stride; only 2 and 2 are defined
+ *           (QNN_ERR_PARAM otherwise).
+ *   y:      {n, floor(Ho/2), floor(Wo/2), m, bits}, Ho x Wo being the
+ *           convolution output size (each at least 2, else QNN_ERR_SHAPE).
+ * Everything else (layouts, limits, errors, streams) as qnn_conv2d.
+ */
+qnn_status qnn_conv2d_maxpool(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
+                              const qnn_conv_geom *g, const qnn_epi *e, int32_t pool_k,
+                              int32_t pool_s, const qnn_tensor *y, void *y_dev, void *stream);
 
 /*
  * Max-pooling on unsigned codes (Sec. IV-A): window kh x kw, strides sh, sw,

@@ -90,6 +90,33 @@ __device__ __forceinline__ uint32_t pack_codes_word(const uint8_t *src)
     }
 }
 
+// Byte-wise maximum of two words of one-byte codes (two 16-bit maxima on
+// the even and the odd bytes).
+__device__ __forceinline__ uint32_t max_bytes(uint32_t a, uint32_t b)
+{
+    typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+    const u16x2 lo = __builtin_elementwise_max(__builtin_bit_cast(u16x2, a & 0x00FF00FFu),
+                                               __builtin_bit_cast(u16x2, b & 0x00FF00FFu));
+    const u16x2 hi = __builtin_elementwise_max(__builtin_bit_cast(u16x2, (a >> 8) & 0x00FF00FFu),
+                                               __builtin_bit_cast(u16x2, (b >> 8) & 0x00FF00FFu));
+    return __builtin_bit_cast(uint32_t, lo) | (__builtin_bit_cast(uint32_t, hi) << 8);
+}
+
+// Code bytes of a 2x2 window: the byte-wise maximum of the four pixels'
+// runs of 32/BITS codes (4 / 8 / 16 bytes), written to out.
+template <int BITS>
+__device__ __forceinline__ void max4_codes(const uint8_t *p00, const uint8_t *p01, const uint8_t *p10,
+                                           const uint8_t *p11, uint8_t *out)
+{
+    constexpr int NW = 8 / BITS;  // 32-bit words of codes
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        const uint32_t a = *(const uint32_t *)(p00 + 4 * i), b = *(const uint32_t *)(p01 + 4 * i);
+        const uint32_t c = *(const uint32_t *)(p10 + 4 * i), d = *(const uint32_t *)(p11 + 4 * i);
+        *(uint32_t *)(out + 4 * i) = max_bytes(max_bytes(a, b), max_bytes(c, d));
+    }
+}
+
 // One output byte from 8/BITS one-byte codes.
 template <int BITS>
 __device__ __forceinline__ uint8_t pack_codes_byte(const uint8_t *src)
@@ -546,7 +573,48 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
         __syncthreads();
 
         // ---- pack the staged codes and copy them out with coalesced stores ----
-        if (a.epi != EPI_RAW32) {
+        if (a.epi != EPI_RAW32 && a.pool) {
+            // fused 2x2 / stride-2 max-pooling: each pooled pixel takes the
+            // byte-wise maximum of its window's codes (windows lie inside the
+            // tile: even tile height and width, or whole images)
+            const int ob0 = m0 * BITS / 8;
+            const int obn = min(a.ot_b, a.ypb - ob0);
+            constexpr int CPW = 32 / BITS;
+            const int thp = a.th >> 1, twp = a.tw >> 1;
+            const int npq = a.ti * thp * twp * a.obq;
+            for (int idx = tid; idx < npq; idx += 256) {
+                const int pp = (int)fdiv((uint32_t)idx, a.div_obq);
+                const int q = idx - pp * a.obq;
+                const int tI = (int)fdiv((uint32_t)pp, a.div_ptile);
+                const int rem = pp - tI * thp * twp;
+                const int pr = (int)fdiv((uint32_t)rem, a.div_ptw);
+                const int pc = rem - pr * twp;
+                const int nn = T.n0 + tI, oy = (T.oy0 >> 1) + pr, ox = (T.ox0 >> 1) + pc;
+                if (nn >= a.n || oy >= a.hp || ox >= a.wp)
+                    continue;
+                const int p00 = tI * a.th * a.tw + 2 * pr * a.tw + 2 * pc;
+                const size_t gp = (size_t)(nn * a.hp + oy) * a.wp + ox;
+                if (a.oquad16) {
+                    if (4 * q < obn) {
+                        __align__(16) uint8_t mx[CPW];
+                        const uint8_t *s0 = sC + p00 * cs + q * CPW;
+                        max4_codes<BITS>(s0, s0 + cs, s0 + a.tw * cs, s0 + (a.tw + 1) * cs, mx);
+                        *(uint32_t *)(a.y + gp * a.ypb + ob0 + 4 * q) = pack_codes_word<BITS>(mx);
+                    }
+                } else if (q < obn) {
+                    // byte-granular tail: 8/BITS codes per output byte
+                    uint32_t b = 0;
+                    const uint8_t *s0 = sC + p00 * cs + q * (8 / BITS);
+#pragma unroll
+                    for (int i = 0; i < 8 / BITS; ++i) {
+                        const uint8_t c0 = max(s0[i], s0[cs + i]);
+                        const uint8_t c1 = max(s0[a.tw * cs + i], s0[(a.tw + 1) * cs + i]);
+                        b |= (uint32_t)max(c0, c1) << (i * BITS);
+                    }
+                    a.y[gp * a.ypb + ob0 + q] = (uint8_t)b;
+                }
+            }
+        } else if (a.epi != EPI_RAW32) {
             const int ob0 = m0 * BITS / 8;
             const int obn = min(a.ot_b, a.ypb - ob0);
             constexpr int CPW = 32 / BITS;  // codes per output word

@@ -132,7 +132,17 @@ int64_t fit_tile(ConvArgs &c, int MT, int PT, int bits, int obits, int64_t w_byt
                  bool code_staging, bool alias = false)
 {
     int ti, th, tw;
-    if ((int64_t)c.ho * c.wo >= PT) {
+    if (c.pool && (int64_t)c.ho * c.wo >= PT) {
+        // pooled tiles hold whole 2x2 windows: an even width (or the whole
+        // row) and an even height (or the rest of the image), at least two rows
+        ti = 1;
+        tw = c.wo <= PT / 2 ? c.wo : PT / 2;
+        th = PT / tw;
+        if (th > c.ho)
+            th = c.ho;
+        if (th < c.ho && (th & 1))
+            th -= 1;
+    } else if ((int64_t)c.ho * c.wo >= PT) {
         ti = 1;
         tw = c.wo < PT ? c.wo : PT;
         th = PT / tw;
@@ -271,13 +281,14 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
 // preferred tile keeps two workgroups per compute unit in the local memory.
 qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16)
 {
-    if (a.m < 32)
+    // fused pooling runs on this kernel whatever the layer's width
+    if (a.m < 32 && !a.pool)
         return QNN_ERR_UNSUPPORTED;
     ConvArgs b = a;
     plan_k_walk(b, al16);
     // measured per layer: the 32x32 kernel wins every layer except 8-bit ones
     // with a K walk along filter rows (pixels of less than 16 bytes)
-    if (bits == 8 && b.row_mode)
+    if (bits == 8 && b.row_mode && !a.pool)
         return QNN_ERR_UNSUPPORTED;
     b.ksteps = 2 * ((b.kchunks + 3) / 4);  // an even number of 32-deep steps
     b.kch = 2 * b.ksteps;
@@ -286,7 +297,8 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16)
     const int obits = b.epi == EPI_RAW32 ? 32 : bits;
     const int64_t tab_bytes = 3 * 4 * (int64_t)b.kch;
     static const int cand[5][2] = {{4, 1}, {2, 2}, {2, 1}, {1, 2}, {1, 1}};
-    for (int pass = 0; pass < 2; ++pass) {
+    // pass 2 (pooled layers only): any tile that fits, even with few tiles
+    for (int pass = 0; pass < (a.pool ? 3 : 2); ++pass) {
         const int64_t lds_cap = pass == 0 ? kLdsBytes / 2 : kLdsBytes;
         for (int i = 0; i < 5; ++i) {
             const int cwm = cand[i][0], cwn = cand[i][1];
@@ -306,7 +318,7 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16)
             if (lds < 0 || lds > lds_cap)
                 continue;
             const int64_t units = (int64_t)c.ntiles * ((c.m + MT - 1) / MT);
-            if (units < 2 * kPlanCus)
+            if (units < 2 * kPlanCus && !(a.pool && pass == 2))
                 continue;
             a = c;
             wm = cwm;
@@ -319,7 +331,7 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16)
 
 qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
                     const qnn_conv_geom *g, const qnn_epi *e, const qnn_tensor *y, void *y_dev,
-                    void *stream)
+                    void *stream, bool pool = false)
 {
     if (!x || !g || !e || !y)
         return QNN_ERR_NULL;
@@ -341,8 +353,14 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     const int32_t wo = out_dim(x->w, g->kw, g->stride_w, g->pad_w);
     if (ho < 1 || wo < 1)
         return QNN_ERR_SHAPE;
-    if (y->n != x->n || y->h != ho || y->w != wo || y->c != m)
+    if (pool) {
+        if (e->kind != QNN_EPI_REQUANT && e->kind != QNN_EPI_STAIR)
+            return QNN_ERR_PARAM;
+        if (ho < 2 || wo < 2 || y->n != x->n || y->h != ho / 2 || y->w != wo / 2 || y->c != m)
+            return QNN_ERR_SHAPE;
+    } else if (y->n != x->n || y->h != ho || y->w != wo || y->c != m) {
         return QNN_ERR_SHAPE;
+    }
     if (y->bits != obits)
         return QNN_ERR_BITS;
     const int64_t pb = pixel_bytes64(x);
@@ -415,8 +433,13 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.clip_lo = e->clip_lo;
     a.clip_hi = e->clip_hi;
     a.ypb = ypb;
+    a.pool = pool ? 1 : 0;
+    a.hp = ho / 2;
+    a.wp = wo / 2;
     int mr = 0, nc = 0, al16 = 0, wm = 0, wn = 0;
     const bool use32 = plan_conv_m32(a, x->bits, wm, wn, al16) == QNN_OK;
+    if (!use32 && pool)
+        return QNN_ERR_UNSUPPORTED;
     if (!use32) {
         st = plan_conv_mfma(a, x->bits, mr, nc, al16);
         if (st != QNN_OK)
@@ -440,11 +463,13 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     }
     a.div_obq = make_fastdiv((uint32_t)a.obq);
     const int MT = use32 ? 32 * wm : 16 * mr;
-    a.contig = a.epi != EPI_RAW32 && a.tw == a.wo && (a.ti == 1 || a.th == a.ho) &&
+    a.contig = a.epi != EPI_RAW32 && !a.pool && a.tw == a.wo && (a.ti == 1 || a.th == a.ho) &&
                a.ot_b == ypb && (ypb % 4) == 0 && m <= MT;
     a.div_qrow = make_fastdiv((uint32_t)(a.wrow / 16 > 0 ? a.wrow / 16 : 1));
     a.div_tab_a = make_fastdiv((uint32_t)(a.row_mode ? a.cpr : (a.c8 >> 4 > 0 ? a.c8 >> 4 : 1)));
     a.div_tab_kw = make_fastdiv((uint32_t)a.kw);
+    a.div_ptile = make_fastdiv((uint32_t)((a.th / 2) * (a.tw / 2) > 0 ? (a.th / 2) * (a.tw / 2) : 1));
+    a.div_ptw = make_fastdiv((uint32_t)(a.tw / 2 > 0 ? a.tw / 2 : 1));
     // words per staged filter row: int8 chunks (16x16 kernel) or packed chunks
     a.div_ncol = make_fastdiv((uint32_t)(use32 ? a.kch * x->bits / 2 : 4 * a.kch));
     st = device_info(&cus);
@@ -549,6 +574,17 @@ qnn_status qnn_conv2d(const qnn_tensor *x, const void *x_dev, int32_t m, const v
                       void *stream)
 {
     return run_conv(x, x_dev, m, w_dev, g, e, y, y_dev, stream);
+}
+
+qnn_status qnn_conv2d_maxpool(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
+                              const qnn_conv_geom *g, const qnn_epi *e, int32_t pool_k,
+                              int32_t pool_s, const qnn_tensor *y, void *y_dev, void *stream)
+{
+    if (pool_k != 2 || pool_s != 2)
+        return QNN_ERR_PARAM;
+    if (x && x->bits == 1)
+        return QNN_ERR_BITS;
+    return run_conv(x, x_dev, m, w_dev, g, e, y, y_dev, stream, true);
 }
 
 qnn_status qnn_linear(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,

@@ -70,6 +70,11 @@ struct ConvArgs {
     int32_t pbq, quad16;   // quads per pixel, 1 if the quad is 16 bytes else 4 bytes
     int32_t ob0, obn, obq, oquad16;  // copy-out byte offset, byte count, quads, quad size flag
     int32_t contig;        // tile = consecutive output pixels with every channel: flat copy-out
+    // fused 2x2 / stride-2 max-pooling of the codes (32x32 kernel): pooled
+    // output size, and divisors of a tile's pooled pixel grid
+    int32_t pool, hp, wp;
+    FastDiv div_ptile;     // (th/2)*(tw/2) pooled pixels per image of a tile
+    FastDiv div_ptw;       // tw/2
 };
 
 // Arguments of the INT-1 XNOR/popcount convolution.

@@ -79,6 +79,9 @@ def lib():
         L.qnn_conv2d.restype = ctypes.c_int
         L.qnn_conv2d.argtypes = [TP, P, ctypes.c_int32, P, ctypes.POINTER(ConvGeom),
                                  ctypes.POINTER(Epi), TP, P, P]
+        L.qnn_conv2d_maxpool.restype = ctypes.c_int
+        L.qnn_conv2d_maxpool.argtypes = [TP, P, ctypes.c_int32, P, ctypes.POINTER(ConvGeom),
+                                         ctypes.POINTER(Epi), ctypes.c_int32, ctypes.c_int32, TP, P, P]
         L.qnn_linear.restype = ctypes.c_int
         L.qnn_linear.argtypes = [TP, P, ctypes.c_int32, P, ctypes.POINTER(Epi), TP, P, P]
         L.qnn_maxpool2d.restype = ctypes.c_int
@@ -169,6 +172,23 @@ def conv2d(x, xshape, bits, w, m, kh, kw, stride=(1, 1), pad=(0, 0), epi="requan
     g = ConvGeom(kh, kw, stride[0], stride[1], pad[0], pad[1])
     _check(lib().qnn_conv2d(ctypes.byref(xd), _ptr(x), m, _ptr(w), ctypes.byref(g), ctypes.byref(e),
                             ctypes.byref(yd), _ptr(y), _stream(stream)), "qnn_conv2d")
+    return y
+
+
+def conv2d_maxpool(x, xshape, bits, w, m, kh, kw, stride=(1, 1), pad=(0, 0), epi="requant",
+                   bias=None, mult=None, shift=None, thresh=None, clip=(0, 0), out=None, stream=None):
+    """Convolution fused with 2x2 / stride-2 max-pooling (qnn_conv2d_maxpool).
+    Returns uint8 [N, floor(Ho/2), floor(Wo/2), out bytes] codes."""
+    n, ho, wo, c, obits = out_shape(xshape, bits, m, kh, kw, stride, pad, epi)
+    yshape = (n, ho // 2, wo // 2, c, obits)
+    y = _out_tensor(yshape, out, x.device)
+    e, _ = _epi(epi, bias, mult, shift, thresh, clip)
+    xd = Tensor(*xshape, bits)
+    yd = Tensor(*yshape)
+    g = ConvGeom(kh, kw, stride[0], stride[1], pad[0], pad[1])
+    _check(lib().qnn_conv2d_maxpool(ctypes.byref(xd), _ptr(x), m, _ptr(w), ctypes.byref(g),
+                                    ctypes.byref(e), 2, 2, ctypes.byref(yd), _ptr(y), _stream(stream)),
+           "qnn_conv2d_maxpool")
     return y
 
 

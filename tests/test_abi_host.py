@@ -25,7 +25,7 @@ def test_exports_every_header_function(q, L):
     assert len(names) >= 12
     for name in names:
         assert hasattr(L, name), name
-    assert L.qnn_abi_version() == 2
+    assert L.qnn_abi_version() == 3
 
 
 def test_status_strings(q, L):
@@ -118,6 +118,31 @@ def test_stair_validation(q, L):
     # a valid call gets past every host check (no GPU here: device error)
     assert call_conv(q, L, (1, 4, 4, 64), 4, 16, g, st4, (1, 4, 4, 16, 4)) == 8
     assert call_conv(q, L, (1, 4, 4, 128), 2, 16, g, st4, (1, 4, 4, 16, 2)) == 8
+
+
+def call_conv_pool(q, L, xs, bits, m, g, epi, ys, pk=2, ps=2, xp=FAKE, wp=FAKE, yp=FAKE):
+    T, G, E = q.qnn.Tensor, q.qnn.ConvGeom, q.qnn.Epi
+    return L.qnn_conv2d_maxpool(ctypes.byref(T(*xs, bits)), xp, m, wp, ctypes.byref(G(*g)),
+                                ctypes.byref(E(*epi)), pk, ps, ctypes.byref(T(*ys)), yp, None)
+
+
+def test_conv_maxpool_validation(q, L):
+    """Fused conv + 2x2/2 max-pool: host checks."""
+    g = (3, 3, 1, 1, 1, 1)
+    ok = ((1, 8, 8, 32), 8, 16, g, REQ8, (1, 4, 4, 16, 8))
+    assert call_conv_pool(q, L, *ok) == 8                               # valid (no GPU here)
+    assert call_conv_pool(q, L, *ok, pk=3) == 4                         # only 2x2 windows
+    assert call_conv_pool(q, L, *ok, ps=1) == 4                         # only stride 2
+    assert call_conv_pool(q, L, (1, 8, 8, 32), 8, 16, g, (2, None, None, None, None, 0, 0),
+                          (1, 4, 4, 16, 32)) == 4                        # RAW32 not pooled
+    assert call_conv_pool(q, L, (1, 8, 8, 32), 8, 16, g, REQ8, (1, 8, 8, 16, 8)) == 3   # unpooled shape
+    assert call_conv_pool(q, L, (1, 7, 9, 32), 8, 16, g, REQ8, (1, 3, 4, 16, 8)) == 8   # floor sizes
+    assert call_conv_pool(q, L, (1, 1, 8, 32), 8, 16, (1, 1, 1, 1, 0, 0), REQ8,
+                          (1, 0, 4, 16, 8)) == 3                         # conv output 1 row
+    assert call_conv_pool(q, L, (1, 8, 8, 256), 1, 16, g, (1, None, None, None, FAKE, 0, 0),
+                          (1, 4, 4, 16, 1)) == 2                         # no INT-1 pooling
+    st = (3, None, None, None, FAKE, 0, 0)
+    assert call_conv_pool(q, L, (2, 6, 6, 64), 4, 40, g, st, (2, 3, 3, 40, 4)) == 8      # staircase
 
 
 def test_unsupported_local_memory(q, L):

@@ -88,7 +88,7 @@ def oracle_network(orc, net, images):
     return logits
 
 
-def gpu_network(qnn, net):
+def gpu_network(qnn, net, fused=True):
     import torch
     from paper_1908_11263_amd.network import cifar_forward
     convs = []
@@ -101,7 +101,7 @@ def gpu_network(qnn, net):
               bias=dev(net.fc_bias), m=10)
     x = dev(net.packed_input())
     cin = net.x_vals.shape[-1]
-    logits = cifar_forward(x, net.n, net.bits, cin, convs, fc, net.clip)
+    logits = cifar_forward(x, net.n, net.bits, cin, convs, fc, net.clip, fused=fused)
     torch.cuda.synchronize()
     return logits.cpu().numpy().reshape(net.n, 10)
 
@@ -111,8 +111,8 @@ def test_cifar_network_small_batch(qnn, orc, bits):
     net = synth.cifar_network(bits=bits, n=5)
     log("case cifar network bits=%d N=5" % bits)
     want = oracle_network(orc, net, np.arange(5))
-    got = gpu_network(qnn, net)
-    assert np.array_equal(got, want)
+    assert np.array_equal(gpu_network(qnn, net), want)
+    assert np.array_equal(gpu_network(qnn, net, fused=False), want)
 
 
 @pytest.mark.parametrize("bits", [8, 4])
