@@ -128,7 +128,9 @@ __device__ __forceinline__ uint8_t pack_codes_byte(const uint8_t *src)
     return (uint8_t)b;
 }
 
-template <int BITS, int WM, int WN, bool AL16>
+// EXT: the staircase epilogue and the fused pooling are compiled in (the
+// plain instances, used by scale-and-clamp and raw layers, carry neither).
+template <int BITS, int WM, int WN, bool AL16, bool EXT>
 __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
 {
     extern __shared__ __align__(16) uint8_t smem[];
@@ -198,7 +200,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     constexpr int NT = BITS == 8 ? 1 : (1 << BITS) - 1;  // staircase thresholds per channel
     auto make_plans = [&](const int32_t *wsum) {
         int mode = 0;
-        if (has_ch && a.epi == EPI_STAIR) {
+        if (EXT && has_ch && a.epi == EPI_STAIR) {
             const bool live = m0 + pch < a.m;
             stair_thresholds(live ? a.thresh + (size_t)(m0 + pch) * NT : nullptr, NT, p_bias, SL,
                              (int32_t *)(sEpi + 4 * pch));
@@ -496,7 +498,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
 #pragma unroll
             for (int t = 0; t < WM; ++t) {
                 const int ch = t * 32 + r32;
-                if (BITS != 8 && a.epi == EPI_STAIR) {
+                if (EXT && BITS != 8 && a.epi == EPI_STAIR) {
                     // staircase (Eq. (4)): count the channel's thresholds at or below acc'
                     int32_t T[16];
 #pragma unroll
@@ -573,7 +575,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
         __syncthreads();
 
         // ---- pack the staged codes and copy them out with coalesced stores ----
-        if (a.epi != EPI_RAW32 && a.pool) {
+        if (EXT && a.epi != EPI_RAW32 && a.pool) {
             // fused 2x2 / stride-2 max-pooling: each pooled pixel takes the
             // byte-wise maximum of its window's codes (windows lie inside the
             // tile: even tile height and width, or whole images)
@@ -675,10 +677,10 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
 template <int BITS>
 hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, dim3 grid, hipStream_t s)
 {
-#define QNN_CASE32(WM_, WN_, AL_)                                                               \
-    if (wm == WM_ && wn == WN_ && al16 == AL_) {                                                \
+#define QNN_CASE32_X(WM_, WN_, AL_, EXT_)                                                       \
+    if (wm == WM_ && wn == WN_ && al16 == AL_ && ext == EXT_) {                                 \
         static bool attr_set = false;                                                           \
-        auto *k = conv_m32_kernel<BITS, WM_, WN_, (AL_ != 0)>;                                  \
+        auto *k = conv_m32_kernel<BITS, WM_, WN_, (AL_ != 0), EXT_>;                            \
         if (!attr_set) {                                                                        \
             if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,  \
                                     a.lds_bytes > 64 * 1024 ? 160 * 1024 : 64 * 1024) != hipSuccess) \
@@ -688,6 +690,8 @@ hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, dim
         hipLaunchKernelGGL(k, grid, dim3(256), a.lds_bytes, s, a);                              \
         return hipGetLastError();                                                               \
     }
+#define QNN_CASE32(WM_, WN_, AL_) QNN_CASE32_X(WM_, WN_, AL_, false) QNN_CASE32_X(WM_, WN_, AL_, true)
+    const bool ext = a.pool != 0 || a.epi == EPI_STAIR;
     QNN_CASE32(1, 1, 0) QNN_CASE32(1, 2, 0) QNN_CASE32(2, 1, 0) QNN_CASE32(2, 2, 0)
     QNN_CASE32(1, 1, 1) QNN_CASE32(1, 2, 1) QNN_CASE32(2, 1, 1) QNN_CASE32(2, 2, 1)
     if constexpr (BITS == 8) {
@@ -696,6 +700,7 @@ hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, dim
         QNN_CASE32(4, 1, 0) QNN_CASE32(4, 1, 1)
     }
 #undef QNN_CASE32
+#undef QNN_CASE32_X
     return hipErrorInvalidValue;
 }
 
