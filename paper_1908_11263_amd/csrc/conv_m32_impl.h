@@ -128,8 +128,9 @@ __device__ __forceinline__ uint8_t pack_codes_byte(const uint8_t *src)
     return (uint8_t)b;
 }
 
-// EXT: the staircase epilogue and the fused pooling are compiled in (the
-// plain instances, used by scale-and-clamp and raw layers, carry neither).
+// EXT: the staircase epilogue, the fused pooling and the next-tile input
+// prefetch are compiled in; the plain instances (scale-and-clamp and raw
+// layers with one tile per workgroup) carry none of them.
 template <int BITS, int WM, int WN, bool AL16, bool EXT>
 __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
 {
@@ -352,6 +353,10 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
 
     const int tile_px = a.ti * a.th * a.tw;
     const int h = lane >> 5, r32 = lane & 31;
+    // next-tile input prefetch (extended instances, which the host picks for
+    // workgroups with more than one tile): for wave tiles of up to two 32x32
+    // MFMA tiles (wider ones would spill the extra registers)
+    constexpr bool PREF = EXT && WM * WN <= 2;
     // code-staging pixel stride (the planner sizes sC with the same value):
     // a compile-time stride turns every staging address into an immediate
     // offset
@@ -361,11 +366,24 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
         if (!first) {
             if (a.alias_out)
                 __syncthreads();  // the previous tile's copy-out still reads sC = sX
-            T = tile_xy(a, tile);
-            if (a.quad16)
-                halo_stage_from<BITS, true, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
-            else
-                halo_stage_from<BITS, false, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
+            // with PREF the first batch of this tile's input arrived in
+            // registers during the previous tile's epilogue; the rest is
+            // staged now
+            if (PREF) {
+                if (a.quad16) {
+                    halo_store<BITS, true, UH>(sX, hq, hd);
+                    halo_stage_from<BITS, true, UH>(a, sX, tid + 256 * UH, T.n0, T.iy0, T.ix0);
+                } else {
+                    halo_store<BITS, false, UH>(sX, hq, hd);
+                    halo_stage_from<BITS, false, UH>(a, sX, tid + 256 * UH, T.n0, T.iy0, T.ix0);
+                }
+            } else {
+                T = tile_xy(a, tile);
+                if (a.quad16)
+                    halo_stage_from<BITS, true, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
+                else
+                    halo_stage_from<BITS, false, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
+            }
             __syncthreads();
         }
 
@@ -451,6 +469,18 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
             __builtin_amdgcn_sched_barrier(0);
             load_frags(2 * pn + 1, o.y, a1, b1);
             __builtin_amdgcn_sched_barrier(0);
+        }
+
+        // the next tile's first input batch is loaded into registers now, so
+        // its latency hides behind this tile's epilogue and copy-out
+        const int next = tile + gridDim.x;
+        TileXY Tn = T;
+        if (PREF && next < a.ntiles) {
+            Tn = tile_xy(a, next);
+            if (a.quad16)
+                halo_issue<BITS, true, UH>(a, tid, totq, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
+            else
+                halo_issue<BITS, false, UH>(a, tid, totq, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
         }
 
         if (a.alias_out)
@@ -671,6 +701,8 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
         }
         // the next tile's input staging overwrites sX / sC only after every
         // wave passed the barrier above; its own barrier follows the staging
+        if (PREF)
+            T = Tn;
     }
 }
 
@@ -691,7 +723,7 @@ hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, dim
         return hipGetLastError();                                                               \
     }
 #define QNN_CASE32(WM_, WN_, AL_) QNN_CASE32_X(WM_, WN_, AL_, false) QNN_CASE32_X(WM_, WN_, AL_, true)
-    const bool ext = a.pool != 0 || a.epi == EPI_STAIR;
+    const bool ext = a.pool != 0 || a.epi == EPI_STAIR || (int64_t)grid.x < a.ntiles;
     QNN_CASE32(1, 1, 0) QNN_CASE32(1, 2, 0) QNN_CASE32(2, 1, 0) QNN_CASE32(2, 2, 0)
     QNN_CASE32(1, 1, 1) QNN_CASE32(1, 2, 1) QNN_CASE32(2, 1, 1) QNN_CASE32(2, 2, 1)
     if constexpr (BITS == 8) {
