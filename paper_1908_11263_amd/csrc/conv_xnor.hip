@@ -98,12 +98,13 @@ __global__ void __launch_bounds__(256) conv_xnor_kernel(const uint32_t *__restri
 
 // Register-resident variant (kd a multiple of 8): a lane gathers its whole
 // im2col column (kd <= KDM words, zero bits for padding taps) once, then
-// walks the output channels of its workgroup's channel group (grid.y; the
-// split keeps several waves per SIMD to hide the scalar-load latency).
-// Channel m's kd filter words arrive by scalar loads, 8 words ahead of their
-// use.  The lane counts mismatching bits, popcount(x ^ w): with K taps of
-// +-1 values, the dot product is K - 2 * mismatches, so no complement is
-// needed (two vector instructions per 32 binary MACs).
+// walks the output channels of its workgroup's channel group (the split
+// over workgroups keeps several waves per SIMD to hide the scalar-load
+// latency).  Channel m's kd filter words arrive by scalar loads one 8-word
+// block ahead of their use.  The lane counts mismatching bits,
+// popcount(x ^ w): with K taps of +-1 values, the dot product is
+// K - 2 * mismatches, so no complement is needed (two vector instructions
+// per 32 binary MACs).
 template <int KDM>
 __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__restrict__ xg,
                                                             const uint32_t *__restrict__ wgl,
@@ -111,7 +112,11 @@ __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__re
                                                             const int32_t *__restrict__ thresh,
                                                             XnorArgs a)
 {
-    const int p = blockIdx.x * 256 + threadIdx.x;
+    // workgroup -> (channel group, pixel block), the group varying fastest:
+    // consecutive workgroups go to different XCDs, so each XCD (and the
+    // scalar caches of its compute units) sees the filters of few groups
+    const int grp = (int)(blockIdx.x % (unsigned)a.ngroups);
+    const int p = (int)(blockIdx.x / (unsigned)a.ngroups) * 256 + threadIdx.x;
     const bool live = p < a.npix;
     const int pc = live ? p : a.npix - 1;
     const int q = (int)fdiv((uint32_t)pc, a.div_wo);
@@ -134,7 +139,7 @@ __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__re
         }
     }
 
-    const int mb = blockIdx.y * a.mgrp;
+    const int mb = grp * a.mgrp;
     const int me = min(a.m, mb + a.mgrp);
     int32_t b_cur = bias ? bias[mb] : 0;
     int32_t t_cur = a.epi == EPI_RAW32 ? 0 : thresh[mb];
@@ -144,29 +149,37 @@ __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__re
         const int mn = m + 1 < me ? m + 1 : m;
         const int32_t b_next = bias ? bias[mn] : 0;
         const int32_t t_next = a.epi == EPI_RAW32 ? 0 : thresh[mn];
-        // kd is a multiple of 8: the filter row is walked in 32-byte blocks;
-        // block b + 1 is fetched while block b is consumed, and the
-        // scheduling barriers keep the compiler from hoisting every block's
-        // scalar loads (which would spill scalar registers).
+        // kd is a multiple of 8: the filter row is walked in 32-byte blocks.
+        // Block b + 1 is requested after the first word of block b is used:
+        // a wait for scalar loads covers every load in flight, so requesting
+        // it earlier would make the wait for block b also wait for b + 1.
+        // The scheduling barriers keep this order (and keep the compiler from
+        // hoisting every block's scalar loads, which would spill scalar
+        // registers).  Each word costs one xor and one accumulating popcount;
+        // the empty asm keeps the additions from being regrouped into
+        // three-input adds, which would cost one more instruction per two
+        // words.
         const uint4 *wr = (const uint4 *)(wgl + (size_t)m * a.kd);
         uint4 c0 = wr[0], c1 = wr[1];
         uint32_t mis = 0;
 #pragma unroll
         for (int kb = 0; kb < KDM; kb += 8) {
             if (kb < a.kd) {
+                const uint32_t w8[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+                mis = __popc(xv[kb] ^ w8[0]) + mis;
+                __asm__("" : "+v"(mis));
+                __builtin_amdgcn_sched_barrier(0);
                 uint4 n0 = c0, n1 = c1;
                 if (kb + 8 < a.kd) {
                     n0 = wr[(kb + 8) / 4];
                     n1 = wr[(kb + 8) / 4 + 1];
                 }
-                mis += __popc(xv[kb + 0] ^ c0.x);
-                mis += __popc(xv[kb + 1] ^ c0.y);
-                mis += __popc(xv[kb + 2] ^ c0.z);
-                mis += __popc(xv[kb + 3] ^ c0.w);
-                mis += __popc(xv[kb + 4] ^ c1.x);
-                mis += __popc(xv[kb + 5] ^ c1.y);
-                mis += __popc(xv[kb + 6] ^ c1.z);
-                mis += __popc(xv[kb + 7] ^ c1.w);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int i = 1; i < 8; ++i) {
+                    mis = __popc(xv[kb + i] ^ w8[i]) + mis;
+                    __asm__("" : "+v"(mis));
+                }
                 c0 = n0;
                 c1 = n1;
             }
@@ -201,7 +214,7 @@ hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s)
 {
     dim3 grid((a.npix + 255) / 256);
     // channel groups of mgrp (a multiple of 32) along grid.y
-    dim3 grid_res(grid.x, (a.m + a.mgrp - 1) / a.mgrp);
+    dim3 grid_res(grid.x * a.ngroups);
     if (a.kd % 8 != 0 || a.kd > 128)
         ;
     else if (a.kd <= 32)

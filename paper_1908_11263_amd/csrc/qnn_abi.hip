@@ -408,6 +408,7 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
             const int64_t maxg = (m + 31) / 32;
             groups = groups < 1 ? 1 : (groups > maxg ? maxg : groups);
             a.mgrp = (int32_t)((((m + groups - 1) / groups) + 31) / 32 * 32);
+            a.ngroups = (m + a.mgrp - 1) / a.mgrp;
         }
         a.div_wo = make_fastdiv((uint32_t)wo);
         a.div_ho = make_fastdiv((uint32_t)ho);

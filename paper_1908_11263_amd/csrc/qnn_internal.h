@@ -88,6 +88,7 @@ struct XnorArgs {
     int32_t kd, kbits, epi, ypb;
     int32_t npix;
     int32_t mgrp;          // output channels per workgroup (multiple of 32), register-resident kernel
+    int32_t ngroups;       // channel groups (ceil(m / mgrp))
     FastDiv div_wo, div_ho, div_cd, div_kw;
 };
 
