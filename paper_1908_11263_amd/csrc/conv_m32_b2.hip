@@ -3,9 +3,9 @@
 
 namespace qnn {
 
-hipError_t launch_conv_m32_b2(const ConvArgs &a, int wm, int wn, int al16, dim3 grid, hipStream_t s)
+hipError_t launch_conv_m32_b2(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s)
 {
-    return launch_conv_m32_bits<2>(a, wm, wn, al16, grid, s);
+    return launch_conv_m32_bits<2>(a, wm, wn, al16, nw, grid, s);
 }
 
 }  // namespace qnn

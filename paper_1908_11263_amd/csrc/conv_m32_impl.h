@@ -131,10 +131,11 @@ __device__ __forceinline__ uint8_t pack_codes_byte(const uint8_t *src)
 // EXT: the staircase epilogue, the fused pooling and the next-tile input
 // prefetch are compiled in; the plain instances (scale-and-clamp and raw
 // layers with one tile per workgroup) carry none of them.
-template <int BITS, int WM, int WN, bool AL16, bool EXT>
-__global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
+template <int BITS, int WM, int WN, bool AL16, bool EXT, int NW>
+__global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
 {
     extern __shared__ __align__(16) uint8_t smem[];
+    constexpr int NT = 64 * NW;   // threads: NW waves of 32*WN pixels each
     constexpr int MT = 32 * WM;
     constexpr int CB = 2 * BITS;  // packed bytes of one 16-byte K chunk
     const int tid = threadIdx.x;
@@ -147,14 +148,14 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     int32_t *sTab = (int32_t *)(smem + a.off_tab);
     int32_t *sNat = sTab + kch;
     int32_t *sVld = sNat + kch;
-    int32_t *sWsum = (int32_t *)(smem + a.off_wsum);            // [MT] filter sums, [4] votes
-    int4 *sEpi = (int4 *)(smem + a.off_wsum + 4 * MT + 16);      // [MT][4]: plan (2) or 16 thresholds
+    int32_t *sWsum = (int32_t *)(smem + a.off_wsum);            // [MT] filter sums, [8] votes
+    int4 *sEpi = (int4 *)(smem + a.off_wsum + 4 * MT + 32);      // [MT][4]: plan (2) or 16 thresholds
     uint8_t *sX = smem + a.off_x;
     uint8_t *sC = smem + a.off_out;                              // [pixel][cs] one byte per code
 
     // ---- prologue: every independent load is issued before any is used ----
-    const int pch = wv + 4 * lane;
-    const bool has_ch = lane < MT / 4;
+    const int pch = wv + NW * lane;
+    const bool has_ch = lane < MT / NW;
     int32_t p_bias = 0, p_mult = 0, p_shift = 0;
     if (has_ch && m0 + pch < a.m) {
         if (a.bias)
@@ -172,12 +173,12 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     // quads of the rows that exist (rows past the last channel stay zero)
     const int nqv = min(MT, a.m - m0) * qrow;
     const uint4 *wsrc = (const uint4 *)(a.w + (size_t)m0 * a.wrow);
-    constexpr int UW = 6;
+    constexpr int UW = NW == 8 ? 3 : 6;
     uint4 wq[UW];
     if (wfast) {
 #pragma unroll
         for (int u = 0; u < UW; ++u) {
-            const int idx = tid + u * 256;
+            const int idx = tid + u * NT;
             wq[u] = make_uint4(0, 0, 0, 0);
             if (idx < nqv)
                 wq[u] = wsrc[idx];
@@ -190,20 +191,20 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     int hd[UH];
     const int totq = a.ti * a.hh * a.hwd * a.pbq;
     if (a.quad16)
-        halo_issue<BITS, true, UH>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
+        halo_issue<BITS, true, UH, NT>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
     else
-        halo_issue<BITS, false, UH>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
+        halo_issue<BITS, false, UH, NT>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
 
     // requantization plans (sub-byte layers: they need no filter sums, so they
     // are computed while the loads above are in flight) and the votes that
     // select a workgroup-uniform epilogue
     constexpr int SL = BITS == 4 ? 4 : (BITS == 2 ? 6 : 0);
-    constexpr int NT = BITS == 8 ? 1 : (1 << BITS) - 1;  // staircase thresholds per channel
+    constexpr int NTH = BITS == 8 ? 1 : (1 << BITS) - 1;  // staircase thresholds per channel
     auto make_plans = [&](const int32_t *wsum) {
         int mode = 0;
         if (EXT && has_ch && a.epi == EPI_STAIR) {
             const bool live = m0 + pch < a.m;
-            stair_thresholds(live ? a.thresh + (size_t)(m0 + pch) * NT : nullptr, NT, p_bias, SL,
+            stair_thresholds(live ? a.thresh + (size_t)(m0 + pch) * NTH : nullptr, NTH, p_bias, SL,
                              (int32_t *)(sEpi + 4 * pch));
             mode = 5;
         } else if (has_ch) {
@@ -234,7 +235,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     // pixel's window in the input tile (sTab, in main-loop order) and at
     // unpacked byte sNat[j] of a filter row; sVld[j] bytes of it are real
     // (the rest pads K)
-    for (int j = tid; j < kch; j += 256) {
+    for (int j = tid; j < kch; j += NT) {
         int hoff = 0, nat = 0, vld = 0;
         if (j < a.kchunks) {
             if (a.row_mode) {
@@ -261,23 +262,23 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     if (wfast) {
 #pragma unroll
         for (int u = 0; u < UW; ++u) {
-            const int idx = tid + u * 256;
+            const int idx = tid + u * NT;
             if (idx < nq) {
                 const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
                 store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
             }
         }
-        for (int b0 = tid + 256 * UW; b0 < nq; b0 += 256 * UW) {
+        for (int b0 = tid + NT * UW; b0 < nq; b0 += NT * UW) {
 #pragma unroll
             for (int u = 0; u < UW; ++u) {
-                const int idx = b0 + u * 256;
+                const int idx = b0 + u * NT;
                 wq[u] = make_uint4(0, 0, 0, 0);
                 if (idx < nqv)
                     wq[u] = wsrc[idx];
             }
 #pragma unroll
             for (int u = 0; u < UW; ++u) {
-                const int idx = b0 + u * 256;
+                const int idx = b0 + u * NT;
                 if (idx < nq) {
                     const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
                     store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
@@ -286,7 +287,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
         }
         // zero the packed bytes of the chunks that round K up to whole steps
         const int padw = (kch - a.kchunks) * CB / 4;
-        for (int i = tid; i < MT * padw; i += 256) {
+        for (int i = tid; i < MT * padw; i += NT) {
             const int row = i / padw;
             *(uint32_t *)(sW + row * a.kp + a.kchunks * CB + 4 * (i - row * padw)) = 0u;
         }
@@ -295,11 +296,11 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
         const int wpr = kch * CB / 4;  // words per staged row
         const int nit = MT * wpr;
         constexpr int U = 4;
-        for (int b0 = tid; b0 < nit; b0 += 256 * U) {
+        for (int b0 = tid; b0 < nit; b0 += NT * U) {
             uint32_t v[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = b0 + u * 256;
+                const int idx = b0 + u * NT;
                 const int row = (int)fdiv((uint32_t)idx, a.div_ncol);
                 const int col = idx - row * wpr;
                 const int j = col / (CB / 4), d = col - j * (CB / 4);
@@ -310,7 +311,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = b0 + u * 256;
+                const int idx = b0 + u * NT;
                 if (idx < nit) {
                     const int row = (int)fdiv((uint32_t)idx, a.div_ncol);
                     *(uint32_t *)(sW + row * a.kp + 4 * (idx - row * wpr)) = v[u];
@@ -321,10 +322,10 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     if (tile < a.ntiles) {
         if (a.quad16) {
             halo_store<BITS, true, UH>(sX, hq, hd);
-            halo_stage_from<BITS, true, UH>(a, sX, tid + 256 * UH, T.n0, T.iy0, T.ix0);
+            halo_stage_from<BITS, true, UH, NT>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
         } else {
             halo_store<BITS, false, UH>(sX, hq, hd);
-            halo_stage_from<BITS, false, UH>(a, sX, tid + 256 * UH, T.n0, T.iy0, T.ix0);
+            halo_stage_from<BITS, false, UH, NT>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
         }
     }
     __syncthreads();
@@ -332,7 +333,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
     // filter sums for the unsigned 8-bit fold, then the 8-bit plans
     if (BITS == 8) {
         const int wpr = kch * 4;
-        for (int row = wv; row < MT; row += 4) {
+        for (int row = wv; row < MT; row += NW) {
             int s = 0;
             for (int col = lane; col < wpr; col += 64) {
                 uint32_t v = *(const uint32_t *)(sW + row * a.kp + col * 4);
@@ -347,7 +348,10 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
         make_plans(sWsum);
         __syncthreads();
     }
-    const int votes = sWsum[MT] & sWsum[MT + 1] & sWsum[MT + 2] & sWsum[MT + 3];
+    int votes = sWsum[MT];
+#pragma unroll
+    for (int w = 1; w < NW; ++w)
+        votes &= sWsum[MT + w];
     const bool all3 = (votes & 4) != 0;
     const bool all4 = (votes & 8) != 0 && !all3;
 
@@ -372,17 +376,17 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
             if (PREF) {
                 if (a.quad16) {
                     halo_store<BITS, true, UH>(sX, hq, hd);
-                    halo_stage_from<BITS, true, UH>(a, sX, tid + 256 * UH, T.n0, T.iy0, T.ix0);
+                    halo_stage_from<BITS, true, UH, NT>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
                 } else {
                     halo_store<BITS, false, UH>(sX, hq, hd);
-                    halo_stage_from<BITS, false, UH>(a, sX, tid + 256 * UH, T.n0, T.iy0, T.ix0);
+                    halo_stage_from<BITS, false, UH, NT>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
                 }
             } else {
                 T = tile_xy(a, tile);
                 if (a.quad16)
-                    halo_stage_from<BITS, true, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
+                    halo_stage_from<BITS, true, UH, NT>(a, sX, tid, T.n0, T.iy0, T.ix0);
                 else
-                    halo_stage_from<BITS, false, UH>(a, sX, tid, T.n0, T.iy0, T.ix0);
+                    halo_stage_from<BITS, false, UH, NT>(a, sX, tid, T.n0, T.iy0, T.ix0);
             }
             __syncthreads();
         }
@@ -478,9 +482,9 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
         if (PREF && next < a.ntiles) {
             Tn = tile_xy(a, next);
             if (a.quad16)
-                halo_issue<BITS, true, UH>(a, tid, totq, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
+                halo_issue<BITS, true, UH, NT>(a, tid, totq, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
             else
-                halo_issue<BITS, false, UH>(a, tid, totq, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
+                halo_issue<BITS, false, UH, NT>(a, tid, totq, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
         }
 
         if (a.alias_out)
@@ -544,7 +548,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
                         uint8_t *dst = sC + (wv * 32 * WN + c * 32 + 4 * h) * cs + ch;
 #pragma unroll
                         for (int v = 0; v < 16; ++v)
-                            dst[(8 * (v >> 2) + (v & 3)) * cs] = (uint8_t)stair_level<NT>((int32_t)acc[t][c][v], T);
+                            dst[(8 * (v >> 2) + (v & 3)) * cs] = (uint8_t)stair_level<NTH>((int32_t)acc[t][c][v], T);
                     }
                     continue;
                 }
@@ -614,7 +618,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
             constexpr int CPW = 32 / BITS;
             const int thp = a.th >> 1, twp = a.tw >> 1;
             const int npq = a.ti * thp * twp * a.obq;
-            for (int idx = tid; idx < npq; idx += 256) {
+            for (int idx = tid; idx < npq; idx += NT) {
                 const int pp = (int)fdiv((uint32_t)idx, a.div_obq);
                 const int q = idx - pp * a.obq;
                 const int tI = (int)fdiv((uint32_t)pp, a.div_ptile);
@@ -661,7 +665,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
                 const int nw = valid * a.obq;
                 if ((a.obq & 3) == 0) {
                     // four words (16 bytes) per store
-                    for (int i4 = tid * 4; i4 < nw; i4 += 256 * 4) {
+                    for (int i4 = tid * 4; i4 < nw; i4 += NT * 4) {
                         const int p = (int)fdiv((uint32_t)i4, a.div_obq);
                         const uint8_t *src = sC + p * cs + (i4 - p * a.obq) * CPW;
                         *(uint4 *)(dst + i4) = make_uint4(pack_codes_word<BITS>(src), pack_codes_word<BITS>(src + CPW),
@@ -669,7 +673,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
                                                           pack_codes_word<BITS>(src + 3 * CPW));
                     }
                 } else {
-                    for (int idx = tid; idx < nw; idx += 256) {
+                    for (int idx = tid; idx < nw; idx += NT) {
                         const int p = (int)fdiv((uint32_t)idx, a.div_obq);
                         const int q = idx - p * a.obq;
                         dst[idx] = pack_codes_word<BITS>(sC + p * cs + q * CPW);
@@ -677,7 +681,7 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
                 }
             } else {
                 const int tq4 = tile_px * a.obq;
-                for (int idx = tid; idx < tq4; idx += 256) {
+                for (int idx = tid; idx < tq4; idx += NT) {
                     const int p = (int)fdiv((uint32_t)idx, a.div_obq);
                     const int q = idx - p * a.obq;
                     const int tI = (int)fdiv((uint32_t)p, a.div_tile_px);
@@ -707,25 +711,28 @@ __global__ void __launch_bounds__(256, 2) conv_m32_kernel(ConvArgs a)
 }
 
 template <int BITS>
-hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, dim3 grid, hipStream_t s)
+hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s)
 {
-#define QNN_CASE32_X(WM_, WN_, AL_, EXT_)                                                       \
-    if (wm == WM_ && wn == WN_ && al16 == AL_ && ext == EXT_) {                                 \
+#define QNN_CASE32_X(WM_, WN_, AL_, EXT_, NW_)                                                  \
+    if (wm == WM_ && wn == WN_ && al16 == AL_ && ext == EXT_ && nw == NW_) {                    \
         static bool attr_set = false;                                                           \
-        auto *k = conv_m32_kernel<BITS, WM_, WN_, (AL_ != 0), EXT_>;                            \
+        auto *k = conv_m32_kernel<BITS, WM_, WN_, (AL_ != 0), EXT_, NW_>;                       \
         if (!attr_set) {                                                                        \
             if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,  \
                                     a.lds_bytes > 64 * 1024 ? 160 * 1024 : 64 * 1024) != hipSuccess) \
                 (void)hipGetLastError();                                                        \
             attr_set = true;                                                                    \
         }                                                                                       \
-        hipLaunchKernelGGL(k, grid, dim3(256), a.lds_bytes, s, a);                              \
+        hipLaunchKernelGGL(k, grid, dim3(64 * NW_), a.lds_bytes, s, a);                         \
         return hipGetLastError();                                                               \
     }
-#define QNN_CASE32(WM_, WN_, AL_) QNN_CASE32_X(WM_, WN_, AL_, false) QNN_CASE32_X(WM_, WN_, AL_, true)
+#define QNN_CASE32(WM_, WN_, AL_) QNN_CASE32_X(WM_, WN_, AL_, false, 4) QNN_CASE32_X(WM_, WN_, AL_, true, 4)
     const bool ext = a.pool != 0 || a.epi == EPI_STAIR || (int64_t)grid.x < a.ntiles;
     QNN_CASE32(1, 1, 0) QNN_CASE32(1, 2, 0) QNN_CASE32(2, 1, 0) QNN_CASE32(2, 2, 0)
     QNN_CASE32(1, 1, 1) QNN_CASE32(1, 2, 1) QNN_CASE32(2, 1, 1) QNN_CASE32(2, 2, 1)
+    // eight-wave workgroups: plain instances for layers with one tile per workgroup
+    QNN_CASE32_X(1, 1, 1, false, 8) QNN_CASE32_X(2, 1, 1, false, 8)
+    QNN_CASE32_X(1, 2, 1, false, 8) QNN_CASE32_X(2, 2, 1, false, 8)
     if constexpr (BITS == 8) {
         // 128-channel wave tiles: 8-bit only (the sub-byte expansion does not fit
         // two workgroups' register budget at this width)

@@ -214,7 +214,7 @@ __device__ __forceinline__ uint32_t stair_level(int32_t acc, const int32_t *T)
 }
 
 // One batch of U packed-input quads of a tile: issue the loads ...
-template <int BITS, bool Q16, int U>
+template <int BITS, bool Q16, int U, int NT = 256>
 __device__ __forceinline__ void halo_issue(const ConvArgs &a, int b0, int totq, int n0, int iy0,
                                            int ix0, uint4 *v, int *dst)
 {
@@ -222,7 +222,7 @@ __device__ __forceinline__ void halo_issue(const ConvArgs &a, int b0, int totq, 
     constexpr int QU = QB * 8 / BITS;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-        const int idx = b0 + u * 256;
+        const int idx = b0 + u * NT;
         v[u] = make_uint4(0, 0, 0, 0);
         dst[u] = -1;
         if (idx < totq) {
@@ -265,15 +265,15 @@ __device__ __forceinline__ void halo_store(uint8_t *sX, const uint4 *v, const in
 }
 
 // Whole tile (or the part after the first batch) in batches of U.
-template <int BITS, bool Q16, int U>
+template <int BITS, bool Q16, int U, int NT = 256>
 __device__ __forceinline__ void halo_stage_from(const ConvArgs &a, uint8_t *sX, int b_first, int n0,
                                                 int iy0, int ix0)
 {
     const int totq = a.ti * a.hh * a.hwd * a.pbq;
-    for (int b0 = b_first; b0 < totq; b0 += 256 * U) {
+    for (int b0 = b_first; b0 < totq; b0 += NT * U) {
         uint4 v[U];
         int dst[U];
-        halo_issue<BITS, Q16, U>(a, b0, totq, n0, iy0, ix0, v, dst);
+        halo_issue<BITS, Q16, U, NT>(a, b0, totq, n0, iy0, ix0, v, dst);
         halo_store<BITS, Q16, U>(sX, v, dst);
     }
 }

@@ -170,7 +170,7 @@ int64_t fit_tile(ConvArgs &c, int MT, int PT, int bits, int obits, int64_t w_byt
     off += tab_bytes;
     off = (off + 15) & ~(int64_t)15;
     const int64_t off_wsum = off;
-    off += 4 * MT + 16 + 64 * MT;   // filter sums, votes, per-channel plans or staircase thresholds
+    off += 4 * MT + 32 + 64 * MT;   // filter sums, votes, per-channel plans or staircase thresholds
     off = (off + 15) & ~(int64_t)15;
     const int64_t off_x = off;
     off += (x_bytes + 15) & ~(int64_t)15;
@@ -279,8 +279,9 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
 // 32x32x32 kernel with packed filters in LDS: used when the layer has at
 // least 32 output channels and enough tiles for two per compute unit; the
 // preferred tile keeps two workgroups per compute unit in the local memory.
-qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16)
+qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int &nw)
 {
+    nw = 4;
     // fused pooling runs on this kernel whatever the layer's width
     if (a.m < 32 && !a.pool)
         return QNN_ERR_UNSUPPORTED;
@@ -323,6 +324,20 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16)
             a = c;
             wm = cwm;
             wn = cwn;
+            // eight waves per workgroup, twice the pixels: for plain layers
+            // whose four-wave plan gives every workgroup a single tile (the
+            // prologue -- filter tile, plans, tables -- is then shared by
+            // twice the work); instantiated for wave tiles of up to 2x2
+            // MFMA tiles with 16-byte aligned fragments
+            if (!a.pool && a.epi != EPI_STAIR && wm <= 2 && al16 &&
+                units <= 2 * kPlanCus) {
+                ConvArgs c8 = b;
+                const int64_t lds8 = fit_tile(c8, MT, 256 * cwn, bits, obits, (int64_t)MT * b.kp, tab_bytes, true);
+                if (lds8 >= 0 && lds8 <= kLdsBytes) {
+                    a = c8;
+                    nw = 8;
+                }
+            }
             return QNN_OK;
         }
     }
@@ -438,7 +453,8 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.hp = ho / 2;
     a.wp = wo / 2;
     int mr = 0, nc = 0, al16 = 0, wm = 0, wn = 0;
-    const bool use32 = plan_conv_m32(a, x->bits, wm, wn, al16) == QNN_OK;
+    int nw = 4;
+    const bool use32 = plan_conv_m32(a, x->bits, wm, wn, al16, nw) == QNN_OK;
     if (!use32 && pool)
         return QNN_ERR_UNSUPPORTED;
     if (!use32) {
@@ -477,7 +493,7 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     if (st != QNN_OK)
         return st;
     const int mtiles = (m + MT - 1) / MT;
-    const int per_cu = a.lds_bytes * 2 <= kLdsBytes ? 2 : 1;
+    const int per_cu = (a.lds_bytes * 2 <= kLdsBytes && nw == 4) ? 2 : 1;
     int64_t gx = (int64_t)cus * per_cu;
     if (gx > a.ntiles)
         gx = a.ntiles;
@@ -487,11 +503,11 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     hipError_t err;
     if (use32) {
         if (x->bits == 8)
-            err = launch_conv_m32_b8(a, wm, wn, al16, grid, s);
+            err = launch_conv_m32_b8(a, wm, wn, al16, nw, grid, s);
         else if (x->bits == 4)
-            err = launch_conv_m32_b4(a, wm, wn, al16, grid, s);
+            err = launch_conv_m32_b4(a, wm, wn, al16, nw, grid, s);
         else
-            err = launch_conv_m32_b2(a, wm, wn, al16, grid, s);
+            err = launch_conv_m32_b2(a, wm, wn, al16, nw, grid, s);
     } else if (x->bits == 8) {
         err = launch_conv_mfma_b8(a, mr, nc, al16, grid, s);
     } else if (x->bits == 4) {
