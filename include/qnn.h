@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define QNN_ABI_VERSION 3
+#define QNN_ABI_VERSION 4
 
 typedef enum {
     QNN_OK = 0,
@@ -111,6 +111,17 @@ typedef struct {
     const int32_t *thresh;   /* [M] (QNN_EPI_THRESH1) or [M][2^b - 1] (QNN_EPI_STAIR) */
     int32_t clip_lo, clip_hi;/* QNN_EPI_REQUANT output range */
 } qnn_epi;
+
+/* Tile shape of the int8-MFMA convolution kernels, for exploration and
+ * tuning (the library otherwise picks it per layer). */
+typedef struct {
+    int32_t kernel;  /* 16: v_mfma_i32_16x16x64_i8 kernel, 32: v_mfma_i32_32x32x32_i8 kernel */
+    int32_t tile_m;  /* MFMA tiles per wave along output channels: 1, 2, 4 (4 at kernel 32: 8 bits only) */
+    int32_t tile_n;  /* MFMA tiles per wave along output pixels: 1, 2, 4 (kernel 32: 1, 2) */
+    int32_t waves;   /* waves per workgroup: 4; or 8 at kernel 32 for scale-and-clamp and raw
+                        layers with 16-byte aligned filter taps, tile_m and tile_n <= 2, when each
+                        workgroup gets a single tile */
+} qnn_tile;
 
 /* Library ABI version (QNN_ABI_VERSION). */
 int32_t qnn_abi_version(void);
@@ -157,6 +168,18 @@ qnn_status qnn_conv2d(const qnn_tensor *x, const void *x_dev, int32_t m, const v
  */
 qnn_status qnn_linear(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
                       const qnn_epi *e, const qnn_tensor *y, void *y_dev, void *stream);
+
+/*
+ * qnn_conv2d with a caller-chosen tile shape (the MI355X counterpart of the
+ * paper's study of register-blocked kernel sizes, Sec. IV-C / Fig. 9):
+ * identical results, different speed.  8-, 4- and 2-bit inputs; shapes that
+ * are not built return QNN_ERR_PARAM, tiles that do not fit the local
+ * memory (or a single-tile eight-wave plan that the device cannot hold)
+ * QNN_ERR_UNSUPPORTED.
+ */
+qnn_status qnn_conv2d_tiled(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
+                            const qnn_conv_geom *g, const qnn_epi *e, const qnn_tile *tile,
+                            const qnn_tensor *y, void *y_dev, void *stream);
 
 /*
  * Convolution fused with the 2x2 / stride-2 max-pooling that follows it in

@@ -234,7 +234,8 @@ void plan_k_walk(ConvArgs &a, int &al16)
 // then widest pixel tile); the first that fits the local memory and gives at
 // least two tiles per compute unit, else the one with the most tiles (small
 // layers are latency-bound and want parallelism).
-qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
+qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16,
+                          const qnn_tile *force = nullptr)
 {
     plan_k_walk(a, al16);
     a.ksteps = (a.kchunks + 3) / 4;
@@ -242,6 +243,16 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
     a.kp = a.ksteps * 64 + 16;
     const int obits = a.epi == EPI_RAW32 ? 32 : bits;
     const int64_t tab_bytes = 3 * 4 * (int64_t)a.kch;
+    if (force) {
+        ConvArgs c = a;
+        if (fit_tile(c, 16 * force->tile_m, 64 * force->tile_n, bits, obits,
+                     (int64_t)16 * force->tile_m * a.kp, tab_bytes, false) < 0)
+            return QNN_ERR_UNSUPPORTED;
+        a = c;
+        mr = force->tile_m;
+        nc = force->tile_n;
+        return QNN_OK;
+    }
     const int mr_first = a.m <= 16 ? 1 : (a.m <= 32 ? 2 : 4);
     ConvArgs best = a;
     int best_mr = 0, best_nc = 0;
@@ -279,17 +290,18 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16)
 // 32x32x32 kernel with packed filters in LDS: used when the layer has at
 // least 32 output channels and enough tiles for two per compute unit; the
 // preferred tile keeps two workgroups per compute unit in the local memory.
-qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int &nw)
+qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int &nw,
+                         bool allow_nw8 = true, const qnn_tile *force = nullptr)
 {
     nw = 4;
     // fused pooling runs on this kernel whatever the layer's width
-    if (a.m < 32 && !a.pool)
+    if (a.m < 32 && !a.pool && !force)
         return QNN_ERR_UNSUPPORTED;
     ConvArgs b = a;
     plan_k_walk(b, al16);
     // measured per layer: the 32x32 kernel wins every layer except 8-bit ones
     // with a K walk along filter rows (pixels of less than 16 bytes)
-    if (bits == 8 && b.row_mode && !a.pool)
+    if (bits == 8 && b.row_mode && !a.pool && !force)
         return QNN_ERR_UNSUPPORTED;
     b.ksteps = 2 * ((b.kchunks + 3) / 4);  // an even number of 32-deep steps
     b.kch = 2 * b.ksteps;
@@ -297,6 +309,25 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
     b.kp = (b.kch + 1) * cb;         // odd multiple of cb: conflict-free fragment reads
     const int obits = b.epi == EPI_RAW32 ? 32 : bits;
     const int64_t tab_bytes = 3 * 4 * (int64_t)b.kch;
+    if (force) {
+        const int MT = 32 * force->tile_m;
+        if (force->waves == 8 && (!al16 || a.pool || a.epi == EPI_STAIR))
+            return QNN_ERR_PARAM;
+        ConvArgs c = b;
+        const int PT = 32 * force->tile_n * force->waves;
+        int64_t lds = fit_tile(c, MT, PT, bits, obits, (int64_t)MT * b.kp, tab_bytes, true);
+        if (lds < 0 || lds > kLdsBytes) {
+            c = b;
+            lds = fit_tile(c, MT, PT, bits, obits, (int64_t)MT * b.kp, tab_bytes, true, true);
+        }
+        if (lds < 0 || lds > kLdsBytes)
+            return QNN_ERR_UNSUPPORTED;
+        a = c;
+        wm = force->tile_m;
+        wn = force->tile_n;
+        nw = force->waves;
+        return QNN_OK;
+    }
     static const int cand[5][2] = {{4, 1}, {2, 2}, {2, 1}, {1, 2}, {1, 1}};
     // pass 2 (pooled layers only): any tile that fits, even with few tiles
     for (int pass = 0; pass < (a.pool ? 3 : 2); ++pass) {
@@ -329,7 +360,7 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
             // prologue -- filter tile, plans, tables -- is then shared by
             // twice the work); instantiated for wave tiles of up to 2x2
             // MFMA tiles with 16-byte aligned fragments
-            if (!a.pool && a.epi != EPI_STAIR && wm <= 2 && al16 &&
+            if (allow_nw8 && !a.pool && a.epi != EPI_STAIR && wm <= 2 && al16 &&
                 units <= 2 * kPlanCus) {
                 ConvArgs c8 = b;
                 const int64_t lds8 = fit_tile(c8, MT, 256 * cwn, bits, obits, (int64_t)MT * b.kp, tab_bytes, true);
@@ -346,7 +377,7 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
 
 qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
                     const qnn_conv_geom *g, const qnn_epi *e, const qnn_tensor *y, void *y_dev,
-                    void *stream, bool pool = false)
+                    void *stream, bool pool = false, const qnn_tile *force = nullptr)
 {
     if (!x || !g || !e || !y)
         return QNN_ERR_NULL;
@@ -454,13 +485,36 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.wp = wo / 2;
     int mr = 0, nc = 0, al16 = 0, wm = 0, wn = 0;
     int nw = 4;
-    const bool use32 = plan_conv_m32(a, x->bits, wm, wn, al16, nw) == QNN_OK;
-    if (!use32 && pool)
-        return QNN_ERR_UNSUPPORTED;
-    if (!use32) {
-        st = plan_conv_mfma(a, x->bits, mr, nc, al16);
+    const ConvArgs a0 = a;
+    bool use32;
+    if (force) {
+        st = force->kernel == 32 ? plan_conv_m32(a, x->bits, wm, wn, al16, nw, false, force)
+                                 : plan_conv_mfma(a, x->bits, mr, nc, al16, force);
         if (st != QNN_OK)
             return st;
+        use32 = force->kernel == 32;
+    } else {
+        use32 = plan_conv_m32(a, x->bits, wm, wn, al16, nw) == QNN_OK;
+        if (!use32 && pool)
+            return QNN_ERR_UNSUPPORTED;
+        if (!use32) {
+            st = plan_conv_mfma(a, x->bits, mr, nc, al16);
+            if (st != QNN_OK)
+                return st;
+        }
+    }
+    st = device_info(&cus);
+    if (st != QNN_OK)
+        return st;
+    if (use32 && nw == 8 && a.ntiles > cus) {
+        // an eight-wave plan needs one tile per workgroup and one workgroup
+        // per compute unit: on a device with fewer compute units the layer
+        // takes four waves
+        if (force)
+            return QNN_ERR_UNSUPPORTED;
+        a = a0;
+        if (plan_conv_m32(a, x->bits, wm, wn, al16, nw, false) != QNN_OK)
+            return QNN_ERR_UNSUPPORTED;
     }
     a.quad16 = (pb % 16) == 0;
     a.pbq = (int32_t)(a.quad16 ? pb / 16 : pb / 4);
@@ -489,9 +543,6 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.div_ptw = make_fastdiv((uint32_t)(a.tw / 2 > 0 ? a.tw / 2 : 1));
     // words per staged filter row: int8 chunks (16x16 kernel) or packed chunks
     a.div_ncol = make_fastdiv((uint32_t)(use32 ? a.kch * x->bits / 2 : 4 * a.kch));
-    st = device_info(&cus);
-    if (st != QNN_OK)
-        return st;
     const int mtiles = (m + MT - 1) / MT;
     const int per_cu = (a.lds_bytes * 2 <= kLdsBytes && nw == 4) ? 2 : 1;
     int64_t gx = (int64_t)cus * per_cu;
@@ -591,6 +642,26 @@ qnn_status qnn_conv2d(const qnn_tensor *x, const void *x_dev, int32_t m, const v
                       void *stream)
 {
     return run_conv(x, x_dev, m, w_dev, g, e, y, y_dev, stream);
+}
+
+qnn_status qnn_conv2d_tiled(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
+                            const qnn_conv_geom *g, const qnn_epi *e, const qnn_tile *tile,
+                            const qnn_tensor *y, void *y_dev, void *stream)
+{
+    if (!tile)
+        return QNN_ERR_NULL;
+    if (x && x->bits == 1)
+        return QNN_ERR_PARAM;  // the binary kernel has no matrix tiles
+    const int tm = tile->tile_m, tn = tile->tile_n;
+    bool built = false;
+    if (tile->kernel == 16)
+        built = tile->waves == 4 && (tm == 1 || tm == 2 || tm == 4) && (tn == 1 || tn == 2 || tn == 4);
+    else if (tile->kernel == 32)
+        built = (tile->waves == 4 || tile->waves == 8) && (tn == 1 || tn == 2) &&
+                (tm == 1 || tm == 2 || (tm == 4 && tn == 1 && tile->waves == 4 && x && x->bits == 8));
+    if (!built)
+        return QNN_ERR_PARAM;
+    return run_conv(x, x_dev, m, w_dev, g, e, y, y_dev, stream, false, tile);
 }
 
 qnn_status qnn_conv2d_maxpool(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,

@@ -44,6 +44,11 @@ class ConvGeom(ctypes.Structure):
                 ("stride_w", ctypes.c_int32), ("pad_h", ctypes.c_int32), ("pad_w", ctypes.c_int32)]
 
 
+class Tile(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_int32), ("tile_m", ctypes.c_int32), ("tile_n", ctypes.c_int32),
+                ("waves", ctypes.c_int32)]
+
+
 class Epi(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("bias", ctypes.c_void_p), ("mult", ctypes.c_void_p),
                 ("shift", ctypes.c_void_p), ("thresh", ctypes.c_void_p),
@@ -79,6 +84,9 @@ def lib():
         L.qnn_conv2d.restype = ctypes.c_int
         L.qnn_conv2d.argtypes = [TP, P, ctypes.c_int32, P, ctypes.POINTER(ConvGeom),
                                  ctypes.POINTER(Epi), TP, P, P]
+        L.qnn_conv2d_tiled.restype = ctypes.c_int
+        L.qnn_conv2d_tiled.argtypes = [TP, P, ctypes.c_int32, P, ctypes.POINTER(ConvGeom),
+                                       ctypes.POINTER(Epi), ctypes.POINTER(Tile), TP, P, P]
         L.qnn_conv2d_maxpool.restype = ctypes.c_int
         L.qnn_conv2d_maxpool.argtypes = [TP, P, ctypes.c_int32, P, ctypes.POINTER(ConvGeom),
                                          ctypes.POINTER(Epi), ctypes.c_int32, ctypes.c_int32, TP, P, P]
@@ -160,18 +168,26 @@ def _out_tensor(shape, out, device):
 
 
 def conv2d(x, xshape, bits, w, m, kh, kw, stride=(1, 1), pad=(0, 0), epi="requant", bias=None,
-           mult=None, shift=None, thresh=None, clip=(0, 0), out=None, stream=None):
+           mult=None, shift=None, thresh=None, clip=(0, 0), out=None, stream=None, tile=None):
     """Quantized convolution (qnn_conv2d).  x: uint8 packed NHWC device tensor
     of logical shape xshape = (n, h, w, c); w: uint8 packed weights.  Returns
-    uint8 [N, Ho, Wo, out bytes] codes or int32 [N, Ho, Wo, M] (raw32)."""
+    uint8 [N, Ho, Wo, out bytes] codes or int32 [N, Ho, Wo, M] (raw32).
+    tile = (kernel, tile_m, tile_n, waves) picks the tile shape
+    (qnn_conv2d_tiled) instead of the library."""
     yshape = out_shape(xshape, bits, m, kh, kw, stride, pad, epi)
     y = _out_tensor(yshape, out, x.device)
     e, _ = _epi(epi, bias, mult, shift, thresh, clip)
     xd = Tensor(*xshape, bits)
     yd = Tensor(*yshape)
     g = ConvGeom(kh, kw, stride[0], stride[1], pad[0], pad[1])
-    _check(lib().qnn_conv2d(ctypes.byref(xd), _ptr(x), m, _ptr(w), ctypes.byref(g), ctypes.byref(e),
-                            ctypes.byref(yd), _ptr(y), _stream(stream)), "qnn_conv2d")
+    if tile is None:
+        _check(lib().qnn_conv2d(ctypes.byref(xd), _ptr(x), m, _ptr(w), ctypes.byref(g),
+                                ctypes.byref(e), ctypes.byref(yd), _ptr(y), _stream(stream)), "qnn_conv2d")
+    else:
+        t = Tile(*tile)
+        _check(lib().qnn_conv2d_tiled(ctypes.byref(xd), _ptr(x), m, _ptr(w), ctypes.byref(g),
+                                      ctypes.byref(e), ctypes.byref(t), ctypes.byref(yd), _ptr(y),
+                                      _stream(stream)), "qnn_conv2d_tiled")
     return y
 
 

@@ -25,7 +25,7 @@ def test_exports_every_header_function(q, L):
     assert len(names) >= 12
     for name in names:
         assert hasattr(L, name), name
-    assert L.qnn_abi_version() == 3
+    assert L.qnn_abi_version() == 4
 
 
 def test_status_strings(q, L):
@@ -143,6 +143,36 @@ def test_conv_maxpool_validation(q, L):
                           (1, 4, 4, 16, 1)) == 2                         # no INT-1 pooling
     st = (3, None, None, None, FAKE, 0, 0)
     assert call_conv_pool(q, L, (2, 6, 6, 64), 4, 40, g, st, (2, 3, 3, 40, 4)) == 8      # staircase
+
+
+def call_conv_tiled(q, L, xs, bits, m, g, epi, ys, tile):
+    T, G, E = q.qnn.Tensor, q.qnn.ConvGeom, q.qnn.Epi
+    return L.qnn_conv2d_tiled(ctypes.byref(T(*xs, bits)), FAKE, m, FAKE, ctypes.byref(G(*g)),
+                              ctypes.byref(E(*epi)), ctypes.byref(q.qnn.Tile(*tile)),
+                              ctypes.byref(T(*ys)), FAKE, None)
+
+
+def test_conv_tiled_validation(q, L):
+    """Caller-chosen tile shapes: only built shapes are accepted."""
+    g = (3, 3, 1, 1, 1, 1)
+    args = ((1, 8, 8, 32), 8, 64, g, REQ8, (1, 8, 8, 64, 8))
+    for tile in [(16, 1, 1, 4), (16, 4, 4, 4), (16, 2, 4, 4), (32, 1, 1, 4), (32, 2, 2, 4),
+                 (32, 4, 1, 4), (32, 2, 1, 8), (32, 1, 2, 8)]:
+        assert call_conv_tiled(q, L, *args, tile) == 8, tile      # valid: no GPU here
+    for tile in [(8, 1, 1, 4), (16, 3, 1, 4), (16, 1, 8, 4), (16, 1, 1, 8), (32, 1, 4, 4),
+                 (32, 4, 2, 4), (32, 4, 1, 8), (32, 1, 1, 2)]:
+        assert call_conv_tiled(q, L, *args, tile) == 4, tile      # shapes that are not built
+    # 128-channel wave tiles of the 32x32 kernel exist at 8 bits only
+    assert call_conv_tiled(q, L, (1, 8, 8, 64), 4, 64, g, (0, None, FAKE, FAKE, None, 0, 15),
+                           (1, 8, 8, 64, 4), (32, 4, 1, 4)) == 4
+    # eight-wave tiles need 16-byte filter taps (C = 4 bytes at 8 bits is a row walk)
+    assert call_conv_tiled(q, L, (1, 8, 8, 4), 8, 32, g, REQ8, (1, 8, 8, 32, 8), (32, 1, 1, 8)) == 4
+    assert call_conv_tiled(q, L, (1, 8, 8, 256), 1, 32, g, (1, None, None, None, FAKE, 0, 0),
+                           (1, 8, 8, 32, 1), (32, 1, 1, 4)) == 4  # no tiles at one bit
+    T, G, E = q.qnn.Tensor, q.qnn.ConvGeom, q.qnn.Epi
+    assert L.qnn_conv2d_tiled(ctypes.byref(T(1, 8, 8, 32, 8)), FAKE, 64, FAKE, ctypes.byref(G(*g)),
+                              ctypes.byref(E(*REQ8)), None, ctypes.byref(T(1, 8, 8, 64, 8)), FAKE,
+                              None) == 1
 
 
 def test_unsupported_local_memory(q, L):
