@@ -72,7 +72,7 @@ class ConvStep:
     """One conv layer with device-resident inputs and preallocated output;
     launch() calls qnn_conv2d through ctypes with prebuilt descriptors."""
 
-    def __init__(self, L, epi=None):
+    def __init__(self, L, epi=None, tile=None):
         import torch
         import paper_1908_11263_amd as qnn
         self.L = L
@@ -91,6 +91,11 @@ class ConvStep:
                      L.m, ctypes.c_void_p(w.data_ptr()),
                      ctypes.byref(q.ConvGeom(L.kh, L.kw, L.stride[0], L.stride[1], L.pad[0], L.pad[1])),
                      ctypes.byref(e), ctypes.byref(q.Tensor(*yshape)), ctypes.c_void_p(self.y.data_ptr())]
+        if tile is not None:
+            # qnn_conv2d_tiled takes the tile descriptor before the output
+            self.tile = q.Tile(*tile)
+            self.args.insert(6, ctypes.byref(self.tile))
+        self.fn = self.lib.qnn_conv2d_tiled if tile is not None else self.lib.qnn_conv2d
         self._refs = (e,)
         self.macs = L.macs
         self.bytes = L.x.nbytes + L.wt.nbytes + self.y.numel() * self.y.element_size() + \
@@ -98,9 +103,14 @@ class ConvStep:
 
     def launch(self):
         import torch
-        st = self.lib.qnn_conv2d(*self.args, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        st = self.fn(*self.args, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
         if st != 0:
-            raise RuntimeError("qnn_conv2d failed with status %d" % st)
+            raise RuntimeError("%s failed with status %d" % (self.fn.__name__, st))
+
+    def try_launch(self):
+        """One launch on the current stream; the status code (0 = launched)."""
+        import torch
+        return self.fn(*self.args, ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
 
 
 class NetworkStep:
@@ -175,6 +185,80 @@ def time_steps(step, steps, warmup, graph=True, per_graph=50):
     return t0.elapsed_time(t1) / 1e3 / steps, steps
 
 
+# Tile shapes built into the library: (kernel, tile_m, tile_n, waves).
+def built_tiles(bits):
+    out = [(16, m, n, 4) for m in (1, 2, 4) for n in (1, 2, 4)]
+    out += [(32, m, n, w) for m in (1, 2) for n in (1, 2) for w in (4, 8)]
+    if bits == 8:
+        out.append((32, 4, 1, 4))
+    return out
+
+
+def tile_model(bits, tile):
+    """Per wave and per K step of the tile: MACs, bytes read from LDS into
+    registers (filter fragments, im2col fragments, the tap-offset table) and
+    VALU ops spent expanding packed filter fragments, from the kernels'
+    main loops.  16x16x64 kernel: every fragment is 64 lanes x 16 int8
+    bytes, one 4-byte table entry per lane per step, weights staged unpacked.
+    32x32x32 kernel: filter fragments stay packed (16*bits/8 bytes per lane)
+    and are expanded in registers (INT-4: 3 ops per packed word, two words;
+    INT-2: 7 ops per word), im2col fragments are 16 bytes per lane, one
+    8-byte table entry per lane per pair of steps."""
+    kern, tm, tn, _ = tile
+    if kern == 16:
+        macs = tm * tn * 16 * 16 * 64
+        lds = 64 * 16 * (tm + tn) + 64 * 4
+        valu = 0
+    else:
+        macs = tm * tn * 32 * 32 * 32
+        lds = 64 * (2 * bits) * tm + 64 * 16 * tn + 64 * 4
+        valu = tm * {8: 0, 4: 6, 2: 7}[bits]
+    return {"macs_per_wave_kstep": macs, "lds_bytes_per_kmac": round(1024.0 * lds / macs, 1),
+            "unpack_valu_per_mfma": round(valu / float(tm * tn), 2),
+            "acc_regs": tm * tn * (4 if kern == 16 else 16)}
+
+
+def tile_sweep(args):
+    """Every built tile shape on the INT-8/4/2 3x3 32x32x64 batch-64 layers
+    and the INT-2 16x16x128 batch-256 layer: one JSON line per (layer, tile)
+    with its time per step (graph replay), throughput, the analytic per-step
+    model and whether the output equals the library's own choice bit for
+    bit; refused shapes carry the status code instead."""
+    import torch
+    import synth
+    layers = [synth.headline_shape_layer(8), synth.int4_layer(), synth.headline_shape_layer(2),
+              synth.int2_layer()]
+    for L in layers:
+        auto = ConvStep(L)
+        graph = not args.no_graph
+        sec, done = time_steps(auto, args.steps, args.warmup, graph=graph)
+        torch.cuda.synchronize()
+        ref = auto.y.clone()
+        rows = [dict(layer=L.name, tile="auto", us=round(sec * 1e6, 3),
+                     gmacs=round(L.macs / sec / 1e9, 1),
+                     pct_int8_mfma_peak=round(100 * 2 * L.macs / sec / 1e12 / PEAK_INT8_TOPS, 2))]
+        for t in built_tiles(L.bits):
+            step = ConvStep(L, tile=t)
+            step.y.fill_(0)
+            st = step.try_launch()
+            torch.cuda.synchronize()
+            row = dict(layer=L.name, tile=list(t), **tile_model(L.bits, t))
+            if st != 0:
+                row["status"] = st
+            else:
+                row["equal_to_auto"] = bool(torch.equal(step.y, ref))
+                sec, done = time_steps(step, args.steps, args.warmup, graph=graph)
+                row.update(us=round(sec * 1e6, 3), gmacs=round(L.macs / sec / 1e9, 1),
+                           pct_int8_mfma_peak=round(100 * 2 * L.macs / sec / 1e12 / PEAK_INT8_TOPS, 2))
+            rows.append(row)
+            log("  %s tile %s: %s" % (L.name, t, "status %d" % st if st else "%.3f us" % row["us"]))
+            del step
+        for r in rows:
+            print(json.dumps(r), flush=True)
+        del auto
+        torch.cuda.empty_cache()
+
+
 def cpu_baseline(L, min_seconds=10.0):
     """The oracle (unchanged) on the host cores over the same INT-4 workload,
     repeated until at least `min_seconds` of wall time."""
@@ -209,6 +293,8 @@ def main():
                     help="run only this workload (int8, int4, int2, int1, cifar8, cifar4) and skip the rest")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-graph", action="store_true", help="launch every step from Python")
+    ap.add_argument("--tile-sweep", action="store_true",
+                    help="time every built tile shape instead (one JSON line per layer and tile)")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="also run one plain device copy of this many bytes (counter calibration)")
     args = ap.parse_args()
@@ -231,6 +317,10 @@ def main():
         b.copy_(a)
         torch.cuda.synchronize()
         log("copy calibration: %d bytes" % args.copy_bytes)
+
+    if args.tile_sweep:
+        tile_sweep(args)
+        return
 
     workloads = {
         "int8": lambda: ConvStep(synth.int8_layer()),

@@ -169,6 +169,17 @@ def int4_layer(n=64):
                       clip=(0, 15))
 
 
+def headline_shape_layer(bits, n=64):
+    """The INT4 layer's shape (3x3, 32x32x64 input, 64 filters, batch n) at
+    8, 4 or 2 bits, for comparing tile shapes across bit-widths."""
+    if bits == 4:
+        return int4_layer(n)
+    hi, wlo = (1 << bits) - 1, -(1 << (bits - 1))
+    return conv_layer("int%d_32x32x64_m64_b%d" % (bits, n), bits, n, 32, 32, 64, 64, 3, 1,
+                      seed=10 + bits, x_rng=(0, hi), w_rng=(wlo, -wlo - 1),
+                      bias_rng=(-16 * hi, 16 * hi), shift={8: 23, 2: 19}[bits], clip=(0, hi))
+
+
 def int4_stair_layer(n=64):
     """The INT4 layer's shape and seed with the staircase epilogue of
     Sec. III-A, Eq. (4): 15 sorted thresholds per channel drawn from
