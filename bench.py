@@ -8,8 +8,9 @@ layer (one launch of the fused conv + requantize + pack kernel) over the
 batch, inputs resident in device memory.  Steps are captured in a HIP graph
 and replayed; the timed region is bracketed by HIP events recorded on the
 stream the kernels run on.  The other workloads (INT-8 batch 1, INT-2 batch
-256, INT-1 batch 1024, the CIFAR-shaped network at INT-8 and INT-4, batch
-4096) are reported under "layers".  The CPU oracle is timed on the host on
+256 on the int8 and on the FP4 matrix path, INT-1 batch 1024, the INT-4
+layer with the staircase epilogue, the CIFAR-shaped network at INT-8 and
+INT-4, batch 4096) are reported under "layers".  The CPU oracle is timed on the host on
 the same INT-4 workload for the "cpu_baseline" object.
 """
 import argparse
@@ -185,12 +186,19 @@ def time_steps(step, steps, warmup, graph=True, per_graph=50):
     return t0.elapsed_time(t1) / 1e3 / steps, steps
 
 
-# Tile shapes built into the library: (kernel, tile_m, tile_n, waves).
+# Tile shapes built into the library: (kernel, tile_m, tile_n, waves);
+# kernel 4 is the INT-2 path on the e2m1 (FP4) matrix instruction.
+TILE_FP4 = 4
+
+
 def built_tiles(bits):
     out = [(16, m, n, 4) for m in (1, 2, 4) for n in (1, 2, 4)]
     out += [(32, m, n, w) for m in (1, 2) for n in (1, 2) for w in (4, 8)]
     if bits == 8:
         out.append((32, 4, 1, 4))
+    if bits == 2:
+        out.append((TILE_FP4, 0, 0, 0))
+        out += [(TILE_FP4, m, n, w) for m in (1, 2) for n in (1, 2) for w in (4, 8)]
     return out
 
 
@@ -203,9 +211,17 @@ def tile_model(bits, tile):
     32x32x32 kernel: filter fragments stay packed (16*bits/8 bytes per lane)
     and are expanded in registers (INT-4: 3 ops per packed word, two words;
     INT-2: 7 ops per word), im2col fragments are 16 bytes per lane, one
-    8-byte table entry per lane per pair of steps."""
+    8-byte table entry per lane per pair of steps.  FP4 kernel (32x32x64
+    e2m1): 16 bytes of nibbles per lane for each operand, no expansion.
+    (The FP4 library pick, tile_m = 0, has no fixed shape.)"""
     kern, tm, tn, _ = tile
-    if kern == 16:
+    if tm == 0:
+        return {}
+    if kern == TILE_FP4:
+        macs = tm * tn * 32 * 32 * 64
+        lds = 64 * 16 * (tm + tn) + 64 * 4
+        valu = 0
+    elif kern == 16:
         macs = tm * tn * 16 * 16 * 64
         lds = 64 * 16 * (tm + tn) + 64 * 4
         valu = 0
@@ -290,7 +306,7 @@ def main():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--only", default=None,
-                    help="run only this workload (int8, int4, int2, int1, cifar8, cifar4) and skip the rest")
+                    help="run only this workload (int8, int4, int2, int2_fp4, int1, int4_stair, cifar8, cifar4)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-graph", action="store_true", help="launch every step from Python")
     ap.add_argument("--tile-sweep", action="store_true",
@@ -326,6 +342,7 @@ def main():
         "int8": lambda: ConvStep(synth.int8_layer()),
         "int4": lambda: ConvStep(synth.int4_layer()),
         "int2": lambda: ConvStep(synth.int2_layer()),
+        "int2_fp4": lambda: ConvStep(synth.int2_layer(), tile=(TILE_FP4, 0, 0, 0)),
         "int1": lambda: ConvStep(synth.int1_layer()),
         "int4_stair": lambda: ConvStep(synth.int4_stair_layer()),
         "cifar8": lambda: NetworkStep(synth.cifar_network(8, n=4096)),

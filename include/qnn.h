@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define QNN_ABI_VERSION 4
+#define QNN_ABI_VERSION 5
 
 typedef enum {
     QNN_OK = 0,
@@ -112,14 +112,27 @@ typedef struct {
     int32_t clip_lo, clip_hi;/* QNN_EPI_REQUANT output range */
 } qnn_epi;
 
-/* Tile shape of the int8-MFMA convolution kernels, for exploration and
+/* qnn_tile.kernel values. */
+#define QNN_TILE_MFMA16 16 /* v_mfma_i32_16x16x64_i8 */
+#define QNN_TILE_MFMA32 32 /* v_mfma_i32_32x32x32_i8 */
+/* INT-2 layers only: v_mfma_scale_f32_32x32x64_f8f6f4 on FP4 (e2m1) operands.
+ * Every INT-2 code is an exact e2m1 value (activations x as x/2, weights w as
+ * w/2, products rescaled by a block exponent of 2) and every partial sum is an
+ * integer below 2^24, so the fp32 accumulator and hence the output equal the
+ * int8 path's bit for bit, at twice the matrix-core rate per instruction.
+ * The library never picks it by itself. */
+#define QNN_TILE_FP4 4
+
+/* Tile shape of the matrix-core convolution kernels, for exploration and
  * tuning (the library otherwise picks it per layer). */
 typedef struct {
-    int32_t kernel;  /* 16: v_mfma_i32_16x16x64_i8 kernel, 32: v_mfma_i32_32x32x32_i8 kernel */
-    int32_t tile_m;  /* MFMA tiles per wave along output channels: 1, 2, 4 (4 at kernel 32: 8 bits only) */
-    int32_t tile_n;  /* MFMA tiles per wave along output pixels: 1, 2, 4 (kernel 32: 1, 2) */
-    int32_t waves;   /* waves per workgroup: 4; or 8 at kernel 32 for scale-and-clamp and raw
-                        layers with 16-byte aligned filter taps, tile_m and tile_n <= 2, when each
+    int32_t kernel;  /* a QNN_TILE_* value */
+    int32_t tile_m;  /* MFMA tiles per wave along output channels: 1, 2, 4 (4 at MFMA32: 8 bits only;
+                        FP4: 1, 2, or 0 with tile_n = waves = 0 to let the library pick) */
+    int32_t tile_n;  /* MFMA tiles per wave along output pixels: 1, 2, 4 (MFMA32, FP4: 1, 2) */
+    int32_t waves;   /* waves per workgroup: 4; or 8 at MFMA32 / FP4 for scale-and-clamp and raw
+                        layers whose filter taps are whole 16-byte chunks of the staged pixel
+                        (channels a multiple of 16; 32 at FP4), tile_m and tile_n <= 2, when each
                         workgroup gets a single tile */
 } qnn_tile;
 
@@ -171,11 +184,14 @@ qnn_status qnn_linear(const qnn_tensor *x, const void *x_dev, int32_t m, const v
 
 /*
  * qnn_conv2d with a caller-chosen tile shape (the MI355X counterpart of the
- * paper's study of register-blocked kernel sizes, Sec. IV-C / Fig. 9):
- * identical results, different speed.  8-, 4- and 2-bit inputs; shapes that
- * are not built return QNN_ERR_PARAM, tiles that do not fit the local
- * memory (or a single-tile eight-wave plan that the device cannot hold)
- * QNN_ERR_UNSUPPORTED.
+ * paper's study of register-blocked kernel sizes, Sec. IV-C / Fig. 9) or
+ * matrix instruction (QNN_TILE_FP4: the sub-byte SIMD the paper's outlook in
+ * Sec. VI asks for, on MI355X's FP4 matrix cores): identical results,
+ * different speed.  8-, 4- and 2-bit inputs (QNN_TILE_FP4: 2-bit only, else
+ * QNN_ERR_BITS; filter volume kh*kw*C above 2796202 QNN_ERR_OVERFLOW);
+ * shapes that are not built return QNN_ERR_PARAM, tiles that do not fit the
+ * local memory (or a single-tile eight-wave plan that the device cannot
+ * hold) QNN_ERR_UNSUPPORTED.
  */
 qnn_status qnn_conv2d_tiled(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
                             const qnn_conv_geom *g, const qnn_epi *e, const qnn_tile *tile,

@@ -20,6 +20,8 @@
 namespace qnn {
 
 typedef int32_t v16i __attribute__((ext_vector_type(16)));
+typedef int32_t v8i __attribute__((ext_vector_type(8)));
+typedef float v16f __attribute__((ext_vector_type(16)));
 
 // Packed form of one A fragment (16 K bytes of one output channel) and its
 // expansion to int8 (4-/2-bit codes scaled by 16 / 64).
@@ -29,6 +31,32 @@ template <> struct PackedA<2> { typedef uint32_t type; };
 
 template <int BITS>
 __device__ __forceinline__ v4i expand_a(v4i p) { return p; }
+
+// FP4 mode (INT-2 layers on the e2m1 matrix instruction): filter fragments
+// are staged as 16 bytes of e2m1 nibbles per lane (no expansion), and the
+// accumulators are fp32 (exact: every partial sum is an integer below 2^24).
+template <bool F4, int BITS> struct FragA { typedef typename PackedA<BITS>::type type; };
+template <int BITS> struct FragA<true, BITS> { typedef v4i type; };
+template <bool F4> struct AccTile { typedef v16i type; };
+template <> struct AccTile<true> { typedef v16f type; };
+
+// One 32x32x64 e2m1 MFMA: rows = A (16 bytes per lane, 32 codes), columns =
+// B; the exponent-2 scale on A restores the factor 1/4 of the x/2, w/2
+// encoding (E8M0 scale bytes: 127 + 2 and 127 + 0).
+__device__ __forceinline__ v16f mfma_f4(v4i a, v4i b, v16f c)
+{
+    const v8i a8 = {a.x, a.y, a.z, a.w, 0, 0, 0, 0};
+    const v8i b8 = {b.x, b.y, b.z, b.w, 0, 0, 0, 0};
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, 129, 0, 127);
+}
+
+// 16 packed INT-2 weight bytes (64 codes) -> 32 bytes of e2m1 nibbles.
+__device__ __forceinline__ void store_w16_f4(uint8_t *dst, uint4 v)
+{
+    const uint2 a = w2_word_f4(v.x), b = w2_word_f4(v.y), c = w2_word_f4(v.z), d = w2_word_f4(v.w);
+    *(uint4 *)dst = make_uint4(a.x, a.y, b.x, b.y);
+    *(uint4 *)(dst + 16) = make_uint4(c.x, c.y, d.x, d.y);
+}
 
 template <int BITS>
 __device__ __forceinline__ v4i expand_a(uint2 d)
@@ -131,13 +159,15 @@ __device__ __forceinline__ uint8_t pack_codes_byte(const uint8_t *src)
 // EXT: the staircase epilogue, the fused pooling and the next-tile input
 // prefetch are compiled in; the plain instances (scale-and-clamp and raw
 // layers with one tile per workgroup) carry none of them.
-template <int BITS, int WM, int WN, bool AL16, bool EXT, int NW>
+template <int BITS, int WM, int WN, bool AL16, bool EXT, int NW, bool F4 = false>
 __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
 {
     extern __shared__ __align__(16) uint8_t smem[];
     constexpr int NT = 64 * NW;   // threads: NW waves of 32*WN pixels each
     constexpr int MT = 32 * WM;
-    constexpr int CB = 2 * BITS;  // packed bytes of one 16-byte K chunk
+    // LDS bytes of one K chunk of a filter row: packed codes (16 K values),
+    // or 16 bytes of e2m1 nibbles (32 K values) in FP4 mode
+    constexpr int CB = F4 ? 16 : 2 * BITS;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wv = tid >> 6;
@@ -191,14 +221,16 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
     int hd[UH];
     const int totq = a.ti * a.hh * a.hwd * a.pbq;
     if (a.quad16)
-        halo_issue<BITS, true, UH, NT>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
+        halo_issue<BITS, true, UH, NT, F4>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
     else
-        halo_issue<BITS, false, UH, NT>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
+        halo_issue<BITS, false, UH, NT, F4>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
 
     // requantization plans (sub-byte layers: they need no filter sums, so they
     // are computed while the loads above are in flight) and the votes that
     // select a workgroup-uniform epilogue
-    constexpr int SL = BITS == 4 ? 4 : (BITS == 2 ? 6 : 0);
+    // log2 of the weight scale the accumulator carries (16 / 64 for packed
+    // 4- / 2-bit fragments; none in FP4 mode, whose block scale removes it)
+    constexpr int SL = F4 ? 0 : (BITS == 4 ? 4 : (BITS == 2 ? 6 : 0));
     constexpr int NTH = BITS == 8 ? 1 : (1 << BITS) - 1;  // staircase thresholds per channel
     auto make_plans = [&](const int32_t *wsum) {
         int mode = 0;
@@ -265,7 +297,10 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
             const int idx = tid + u * NT;
             if (idx < nq) {
                 const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
-                store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
+                if (F4)
+                    store_w16_f4(sW + row * a.kp + (idx - row * qrow) * 32, wq[u]);
+                else
+                    store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
             }
         }
         for (int b0 = tid + NT * UW; b0 < nq; b0 += NT * UW) {
@@ -281,7 +316,10 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 const int idx = b0 + u * NT;
                 if (idx < nq) {
                     const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
-                    store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
+                    if (F4)
+                        store_w16_f4(sW + row * a.kp + (idx - row * qrow) * 32, wq[u]);
+                    else
+                        store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
                 }
             }
         }
@@ -292,8 +330,10 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
             *(uint32_t *)(sW + row * a.kp + a.kchunks * CB + 4 * (i - row * padw)) = 0u;
         }
     } else {
-        // general order (row walk for small C): one packed 4-byte word per item
-        const int wpr = kch * CB / 4;  // words per staged row
+        // general order (row walk for small C): one packed 4-byte word per
+        // item, staged as IB bytes (itself, or 8 bytes of e2m1 nibbles)
+        constexpr int IB = F4 ? 8 : 4;
+        const int wpr = kch * CB / IB;  // items per staged row
         const int nit = MT * wpr;
         constexpr int U = 4;
         for (int b0 = tid; b0 < nit; b0 += NT * U) {
@@ -303,29 +343,35 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 const int idx = b0 + u * NT;
                 const int row = (int)fdiv((uint32_t)idx, a.div_ncol);
                 const int col = idx - row * wpr;
-                const int j = col / (CB / 4), d = col - j * (CB / 4);
+                const int j = col / (CB / IB), d = col - j * (CB / IB);
                 const int mg = m0 + row;
+                // the chunk's packed offset in the filter row and its real bytes
+                const int pnat = F4 ? sNat[j] / 2 : sNat[j] * BITS / 8;
+                const int pvld = F4 ? sVld[j] / 2 : sVld[j] * BITS / 8;
                 v[u] = 0;
-                if (idx < nit && mg < a.m && 4 * d < sVld[j] * BITS / 8)
-                    v[u] = *(const uint32_t *)(a.w + (size_t)mg * a.wrow + sNat[j] * BITS / 8 + 4 * d);
+                if (idx < nit && mg < a.m && 4 * d < pvld)
+                    v[u] = *(const uint32_t *)(a.w + (size_t)mg * a.wrow + pnat + 4 * d);
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int idx = b0 + u * NT;
                 if (idx < nit) {
                     const int row = (int)fdiv((uint32_t)idx, a.div_ncol);
-                    *(uint32_t *)(sW + row * a.kp + 4 * (idx - row * wpr)) = v[u];
+                    if (F4)
+                        *(uint2 *)(sW + row * a.kp + 8 * (idx - row * wpr)) = w2_word_f4(v[u]);
+                    else
+                        *(uint32_t *)(sW + row * a.kp + 4 * (idx - row * wpr)) = v[u];
                 }
             }
         }
     }
     if (tile < a.ntiles) {
         if (a.quad16) {
-            halo_store<BITS, true, UH>(sX, hq, hd);
-            halo_stage_from<BITS, true, UH, NT>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
+            halo_store<BITS, true, UH, F4>(sX, hq, hd);
+            halo_stage_from<BITS, true, UH, NT, F4>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
         } else {
-            halo_store<BITS, false, UH>(sX, hq, hd);
-            halo_stage_from<BITS, false, UH, NT>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
+            halo_store<BITS, false, UH, F4>(sX, hq, hd);
+            halo_stage_from<BITS, false, UH, NT, F4>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
         }
     }
     __syncthreads();
@@ -353,7 +399,6 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
     for (int w = 1; w < NW; ++w)
         votes &= sWsum[MT + w];
     const bool all3 = (votes & 4) != 0;
-    const bool all4 = (votes & 8) != 0 && !all3;
 
     const int tile_px = a.ti * a.th * a.tw;
     const int h = lane >> 5, r32 = lane & 31;
@@ -375,18 +420,18 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
             // staged now
             if (PREF) {
                 if (a.quad16) {
-                    halo_store<BITS, true, UH>(sX, hq, hd);
-                    halo_stage_from<BITS, true, UH, NT>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
+                    halo_store<BITS, true, UH, F4>(sX, hq, hd);
+                    halo_stage_from<BITS, true, UH, NT, F4>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
                 } else {
-                    halo_store<BITS, false, UH>(sX, hq, hd);
-                    halo_stage_from<BITS, false, UH, NT>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
+                    halo_store<BITS, false, UH, F4>(sX, hq, hd);
+                    halo_stage_from<BITS, false, UH, NT, F4>(a, sX, tid + NT * UH, T.n0, T.iy0, T.ix0);
                 }
             } else {
                 T = tile_xy(a, tile);
                 if (a.quad16)
-                    halo_stage_from<BITS, true, UH, NT>(a, sX, tid, T.n0, T.iy0, T.ix0);
+                    halo_stage_from<BITS, true, UH, NT, F4>(a, sX, tid, T.n0, T.iy0, T.ix0);
                 else
-                    halo_stage_from<BITS, false, UH, NT>(a, sX, tid, T.n0, T.iy0, T.ix0);
+                    halo_stage_from<BITS, false, UH, NT, F4>(a, sX, tid, T.n0, T.iy0, T.ix0);
             }
             __syncthreads();
         }
@@ -408,17 +453,18 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 base[c] = ((tI * a.hh + py * a.sh) * a.hwd + px * a.sw) * a.ps;
             }
         }
-        v16i acc[WM][WN];
+        typedef typename AccTile<F4>::type ACC;
+        ACC acc[WM][WN];
 #pragma unroll
         for (int t = 0; t < WM; ++t)
 #pragma unroll
             for (int c = 0; c < WN; ++c)
-                acc[t][c] = (v16i){};
+                acc[t][c] = (ACC){};
         const uint8_t *aRow = sW + r32 * a.kp + h * CB;
         // filter fragments are read in packed form (2 / 1 registers for 4 / 2
         // bits) and expanded right before their MFMAs; two register sets
         // alternate, so the reads of step k+1 are in flight during step k
-        typedef typename PackedA<BITS>::type PA;
+        typedef typename FragA<F4, BITS>::type PA;
         auto load_frags = [&](int ks, int off, PA *A, v4i *B) {
 #pragma unroll
             for (int t = 0; t < WM; ++t)
@@ -439,8 +485,12 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
             for (int t = 0; t < WM; ++t) {
                 const v4i av = expand_a<BITS>(A[t]);
 #pragma unroll
-                for (int c = 0; c < WN; ++c)
-                    acc[t][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(B[c], av, acc[t][c], 0, 0, 0);
+                for (int c = 0; c < WN; ++c) {
+                    if constexpr (F4)
+                        acc[t][c] = mfma_f4(B[c], av, acc[t][c]);
+                    else
+                        acc[t][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(B[c], av, acc[t][c], 0, 0, 0);
+                }
             }
         };
         // K steps come in pairs (the planner rounds them up to an even count);
@@ -482,9 +532,9 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
         if (PREF && next < a.ntiles) {
             Tn = tile_xy(a, next);
             if (a.quad16)
-                halo_issue<BITS, true, UH, NT>(a, tid, totq, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
+                halo_issue<BITS, true, UH, NT, F4>(a, tid, totq, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
             else
-                halo_issue<BITS, false, UH, NT>(a, tid, totq, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
+                halo_issue<BITS, false, UH, NT, F4>(a, tid, totq, Tn.n0, Tn.iy0, Tn.ix0, hq, hd);
         }
 
         if (a.alias_out)
@@ -517,11 +567,7 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                         const int nn = T.n0 + tI, oy = T.oy0 + py, ox = T.ox0 + px;
                         if (nn >= a.n || oy >= a.ho || ox >= a.wo)
                             continue;
-                        int32_t acc32 = acc[t][c][v];
-                        if (BITS == 4)
-                            acc32 >>= 4;
-                        else if (BITS == 2)
-                            acc32 >>= 6;
+                        const int32_t acc32 = (int32_t)acc[t][c][v] >> SL;
                         const size_t gp = (size_t)(nn * a.ho + oy) * a.wo + ox;
                         ((int32_t *)a.y)[gp * a.m + mg] = (int32_t)(uint32_t)(uint64_t)(acc32 + bt);
                     }
@@ -569,7 +615,7 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                     } else {
 #pragma unroll
                         for (int v = 0; v < 16; ++v) {
-                            const int32_t accd = acc[t][c][v];
+                            const int32_t accd = (int32_t)acc[t][c][v];
                             uint32_t code;
                             if (e1.z >= 3) {
                                 const int32_t d = __builtin_elementwise_sub_sat(accd, e0.x);
@@ -577,11 +623,7 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                                 const uint64_t rs = ((uint64_t)(uint32_t)e1.y << 32) | (uint32_t)e0.w;
                                 code = (uint32_t)(((uint64_t)dc * (uint32_t)e0.z + rs) >> e1.x);
                             } else {
-                                int32_t acc32 = accd;
-                                if (BITS == 4)
-                                    acc32 >>= 4;
-                                else if (BITS == 2)
-                                    acc32 >>= 6;
+                                const int32_t acc32 = accd >> SL;
                                 int64_t r;
                                 if (e1.z) {
                                     const int32_t d = __builtin_elementwise_sub_sat(acc32, e0.x);
@@ -710,13 +752,13 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
     }
 }
 
-template <int BITS>
+template <int BITS, bool F4 = false>
 hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s)
 {
 #define QNN_CASE32_X(WM_, WN_, AL_, EXT_, NW_)                                                  \
     if (wm == WM_ && wn == WN_ && al16 == AL_ && ext == EXT_ && nw == NW_) {                    \
         static bool attr_set = false;                                                           \
-        auto *k = conv_m32_kernel<BITS, WM_, WN_, (AL_ != 0), EXT_, NW_>;                       \
+        auto *k = conv_m32_kernel<BITS, WM_, WN_, (AL_ != 0), EXT_, NW_, F4>;                   \
         if (!attr_set) {                                                                        \
             if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,  \
                                     a.lds_bytes > 64 * 1024 ? 160 * 1024 : 64 * 1024) != hipSuccess) \
@@ -733,7 +775,7 @@ hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, int
     // eight-wave workgroups: plain instances for layers with one tile per workgroup
     QNN_CASE32_X(1, 1, 1, false, 8) QNN_CASE32_X(2, 1, 1, false, 8)
     QNN_CASE32_X(1, 2, 1, false, 8) QNN_CASE32_X(2, 2, 1, false, 8)
-    if constexpr (BITS == 8) {
+    if constexpr (BITS == 8 && !F4) {
         // 128-channel wave tiles: 8-bit only (the sub-byte expansion does not fit
         // two workgroups' register budget at this width)
         QNN_CASE32(4, 1, 0) QNN_CASE32(4, 1, 1)

@@ -59,6 +59,33 @@ __device__ __forceinline__ void stage_word(uint8_t *dst, uint32_t v)
     }
 }
 
+// INT-2 codes as FP4 (OCP e2m1: sign, 2-bit exponent with bias 1, 1-bit
+// mantissa) for the 32x32x64 f8f6f4 matrix instruction.  The nibbles 0000,
+// 0001, 0010, 0011 encode 0, 0.5, 1, 1.5, so an activation code x placed in
+// a nibble IS the e2m1 value x/2; a weight code (two's complement b1 b0)
+// becomes w/2: 01 -> 0001 (0.5), 10 -> 1010 (-1), 11 -> 1001 (-0.5).  Every
+// product is then x*w/4, restored by an exponent-2 block scale.  One packed
+// word (16 codes) -> 8 bytes: the even-position codes c0 c2 .. c14 in the low
+// word's nibbles 0..7 and the odd ones in the high word's (the same order for
+// weights and activations, so the dot products are unchanged).
+__device__ __forceinline__ uint2 x2_word_f4(uint32_t v)
+{
+    return make_uint2(v & 0x33333333u, (v >> 2) & 0x33333333u);
+}
+
+__device__ __forceinline__ uint32_t w2_nibbles_f4(uint32_t t)
+{
+    const uint32_t o = t & 0x11111111u;  // b0 of every nibble
+    const uint32_t s = t & 0x22222222u;  // b1 (the sign) of every nibble
+    return (s << 2) | (s & ~(o << 1)) | o;
+}
+
+__device__ __forceinline__ uint2 w2_word_f4(uint32_t v)
+{
+    const uint2 t = x2_word_f4(v);
+    return make_uint2(w2_nibbles_f4(t.x), w2_nibbles_f4(t.y));
+}
+
 // Weights, one packed word -> 8 (INT-4) or 16 (INT-2) bytes holding 16*w /
 // 64*w: the code moved to the top of its byte is exactly that signed byte.
 __device__ __forceinline__ uint2 w4_word(uint32_t v)
@@ -214,12 +241,13 @@ __device__ __forceinline__ uint32_t stair_level(int32_t acc, const int32_t *T)
 }
 
 // One batch of U packed-input quads of a tile: issue the loads ...
-template <int BITS, bool Q16, int U, int NT = 256>
+// (F4: INT-2 codes staged as e2m1 nibbles, 4 bits per code, instead of bytes)
+template <int BITS, bool Q16, int U, int NT = 256, bool F4 = false>
 __device__ __forceinline__ void halo_issue(const ConvArgs &a, int b0, int totq, int n0, int iy0,
                                            int ix0, uint4 *v, int *dst)
 {
     constexpr int QB = Q16 ? 16 : 4;
-    constexpr int QU = QB * 8 / BITS;
+    constexpr int QU = QB * (F4 ? 4 : 8) / BITS;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int idx = b0 + u * NT;
@@ -246,14 +274,25 @@ __device__ __forceinline__ void halo_issue(const ConvArgs &a, int b0, int totq, 
 }
 
 // ... and unpack them into the LDS tile.
-template <int BITS, bool Q16, int U>
+template <int BITS, bool Q16, int U, bool F4 = false>
 __device__ __forceinline__ void halo_store(uint8_t *sX, const uint4 *v, const int *dst)
 {
-    constexpr int W = 32 / BITS;  // unpacked bytes per packed word
+    constexpr int W = (F4 ? 16 : 32) / BITS;  // staged bytes per packed word
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         if (dst[u] >= 0) {
             uint8_t *d = sX + dst[u];
+            if (F4) {
+                const uint2 p = x2_word_f4(v[u].x);
+                if (Q16) {
+                    const uint2 q = x2_word_f4(v[u].y), r = x2_word_f4(v[u].z), t = x2_word_f4(v[u].w);
+                    *(uint4 *)d = make_uint4(p.x, p.y, q.x, q.y);
+                    *(uint4 *)(d + 16) = make_uint4(r.x, r.y, t.x, t.y);
+                } else {
+                    *(uint2 *)d = p;
+                }
+                continue;
+            }
             stage_word<BITS>(d, v[u].x);
             if (Q16) {
                 stage_word<BITS>(d + W, v[u].y);
@@ -265,7 +304,7 @@ __device__ __forceinline__ void halo_store(uint8_t *sX, const uint4 *v, const in
 }
 
 // Whole tile (or the part after the first batch) in batches of U.
-template <int BITS, bool Q16, int U, int NT = 256>
+template <int BITS, bool Q16, int U, int NT = 256, bool F4 = false>
 __device__ __forceinline__ void halo_stage_from(const ConvArgs &a, uint8_t *sX, int b_first, int n0,
                                                 int iy0, int ix0)
 {
@@ -273,8 +312,8 @@ __device__ __forceinline__ void halo_stage_from(const ConvArgs &a, uint8_t *sX, 
     for (int b0 = b_first; b0 < totq; b0 += NT * U) {
         uint4 v[U];
         int dst[U];
-        halo_issue<BITS, Q16, U, NT>(a, b0, totq, n0, iy0, ix0, v, dst);
-        halo_store<BITS, Q16, U>(sX, v, dst);
+        halo_issue<BITS, Q16, U, NT, F4>(a, b0, totq, n0, iy0, ix0, v, dst);
+        halo_store<BITS, Q16, U, F4>(sX, v, dst);
     }
 }
 

@@ -290,12 +290,15 @@ qnn_status plan_conv_mfma(ConvArgs &a, int bits, int &mr, int &nc, int &al16,
 // 32x32x32 kernel with packed filters in LDS: used when the layer has at
 // least 32 output channels and enough tiles for two per compute unit; the
 // preferred tile keeps two workgroups per compute unit in the local memory.
+// f4: INT-2 layer on the e2m1 instruction (filter rows staged as 16 bytes of
+// nibbles per 32-deep K chunk, like an 8-bit layer of half the channels).
 qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int &nw,
-                         bool allow_nw8 = true, const qnn_tile *force = nullptr)
+                         bool allow_nw8 = true, const qnn_tile *force = nullptr, bool f4 = false)
 {
     nw = 4;
-    // fused pooling runs on this kernel whatever the layer's width
-    if (a.m < 32 && !a.pool && !force)
+    // fused pooling runs on this kernel whatever the layer's width, and so
+    // does the e2m1 path (chosen by the caller)
+    if (a.m < 32 && !a.pool && !force && !f4)
         return QNN_ERR_UNSUPPORTED;
     ConvArgs b = a;
     plan_k_walk(b, al16);
@@ -305,7 +308,7 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
         return QNN_ERR_UNSUPPORTED;
     b.ksteps = 2 * ((b.kchunks + 3) / 4);  // an even number of 32-deep steps
     b.kch = 2 * b.ksteps;
-    const int cb = 2 * bits;         // packed bytes per 16-byte K chunk
+    const int cb = f4 ? 16 : 2 * bits;  // LDS bytes of a filter row per 16-byte K chunk
     b.kp = (b.kch + 1) * cb;         // odd multiple of cb: conflict-free fragment reads
     const int obits = b.epi == EPI_RAW32 ? 32 : bits;
     const int64_t tab_bytes = 3 * 4 * (int64_t)b.kch;
@@ -329,8 +332,10 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
         return QNN_OK;
     }
     static const int cand[5][2] = {{4, 1}, {2, 2}, {2, 1}, {1, 2}, {1, 1}};
-    // pass 2 (pooled layers only): any tile that fits, even with few tiles
-    for (int pass = 0; pass < (a.pool ? 3 : 2); ++pass) {
+    // pass 2 (pooled layers and the e2m1 path, which have no other kernel to
+    // fall back on): any tile that fits, even with few tiles
+    const bool last_resort = a.pool || f4;
+    for (int pass = 0; pass < (last_resort ? 3 : 2); ++pass) {
         const int64_t lds_cap = pass == 0 ? kLdsBytes / 2 : kLdsBytes;
         for (int i = 0; i < 5; ++i) {
             const int cwm = cand[i][0], cwn = cand[i][1];
@@ -350,7 +355,7 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
             if (lds < 0 || lds > lds_cap)
                 continue;
             const int64_t units = (int64_t)c.ntiles * ((c.m + MT - 1) / MT);
-            if (units < 2 * kPlanCus && !(a.pool && pass == 2))
+            if (units < 2 * kPlanCus && !(last_resort && pass == 2))
                 continue;
             a = c;
             wm = cwm;
@@ -414,6 +419,12 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
         return QNN_ERR_ALIGN;
     const int64_t K = (int64_t)g->kh * g->kw * x->c;
     if (K > max_k_for(x->bits))
+        return QNN_ERR_OVERFLOW;
+    // the e2m1 path: INT-2 codes staged as nibbles, half a byte per channel;
+    // its fp32 accumulation is exact while every partial sum stays below 2^24
+    // in magnitude (|x * w| <= 3 * 2 per term)
+    const bool f4 = force && force->kernel == QNN_TILE_FP4;
+    if (f4 && K * 6 > ((int64_t)1 << 24))
         return QNN_ERR_OVERFLOW;
     if ((int64_t)x->n * ho * wo >= ((int64_t)1 << 31) || (int64_t)x->n * x->h * x->w >= ((int64_t)1 << 31))
         return QNN_ERR_SHAPE;
@@ -485,9 +496,18 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.wp = wo / 2;
     int mr = 0, nc = 0, al16 = 0, wm = 0, wn = 0;
     int nw = 4;
+    if (f4)
+        a.c8 = x->c / 2;
     const ConvArgs a0 = a;
     bool use32;
-    if (force) {
+    if (f4) {
+        // tile_m = 0: the library picks the tile, as for qnn_conv2d
+        st = plan_conv_m32(a, x->bits, wm, wn, al16, nw, force->tile_m == 0,
+                           force->tile_m == 0 ? nullptr : force, true);
+        if (st != QNN_OK)
+            return st;
+        use32 = true;
+    } else if (force) {
         st = force->kernel == 32 ? plan_conv_m32(a, x->bits, wm, wn, al16, nw, false, force)
                                  : plan_conv_mfma(a, x->bits, mr, nc, al16, force);
         if (st != QNN_OK)
@@ -510,10 +530,10 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
         // an eight-wave plan needs one tile per workgroup and one workgroup
         // per compute unit: on a device with fewer compute units the layer
         // takes four waves
-        if (force)
+        if (force && !(f4 && force->tile_m == 0))
             return QNN_ERR_UNSUPPORTED;
         a = a0;
-        if (plan_conv_m32(a, x->bits, wm, wn, al16, nw, false) != QNN_OK)
+        if (plan_conv_m32(a, x->bits, wm, wn, al16, nw, false, nullptr, f4) != QNN_OK)
             return QNN_ERR_UNSUPPORTED;
     }
     a.quad16 = (pb % 16) == 0;
@@ -541,8 +561,9 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.div_tab_kw = make_fastdiv((uint32_t)a.kw);
     a.div_ptile = make_fastdiv((uint32_t)((a.th / 2) * (a.tw / 2) > 0 ? (a.th / 2) * (a.tw / 2) : 1));
     a.div_ptw = make_fastdiv((uint32_t)(a.tw / 2 > 0 ? a.tw / 2 : 1));
-    // words per staged filter row: int8 chunks (16x16 kernel) or packed chunks
-    a.div_ncol = make_fastdiv((uint32_t)(use32 ? a.kch * x->bits / 2 : 4 * a.kch));
+    // staging items per filter row: int8 words (16x16 kernel), packed words,
+    // or 8-byte e2m1 groups (one packed word each)
+    a.div_ncol = make_fastdiv((uint32_t)(f4 ? 2 * a.kch : (use32 ? a.kch * x->bits / 2 : 4 * a.kch)));
     const int mtiles = (m + MT - 1) / MT;
     const int per_cu = (a.lds_bytes * 2 <= kLdsBytes && nw == 4) ? 2 : 1;
     int64_t gx = (int64_t)cus * per_cu;
@@ -552,7 +573,9 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
         gx = 1;
     dim3 grid((unsigned)gx, (unsigned)mtiles);
     hipError_t err;
-    if (use32) {
+    if (f4) {
+        err = launch_conv_m32_f4(a, wm, wn, al16, nw, grid, s);
+    } else if (use32) {
         if (x->bits == 8)
             err = launch_conv_m32_b8(a, wm, wn, al16, nw, grid, s);
         else if (x->bits == 4)
@@ -654,7 +677,12 @@ qnn_status qnn_conv2d_tiled(const qnn_tensor *x, const void *x_dev, int32_t m, c
         return QNN_ERR_PARAM;  // the binary kernel has no matrix tiles
     const int tm = tile->tile_m, tn = tile->tile_n;
     bool built = false;
-    if (tile->kernel == 16)
+    if (tile->kernel == QNN_TILE_FP4) {
+        if (x && x->bits != 2)
+            return QNN_ERR_BITS;
+        built = (tm == 0 && tn == 0 && tile->waves == 0) ||
+                ((tile->waves == 4 || tile->waves == 8) && (tn == 1 || tn == 2) && (tm == 1 || tm == 2));
+    } else if (tile->kernel == 16)
         built = tile->waves == 4 && (tm == 1 || tm == 2 || tm == 4) && (tn == 1 || tn == 2 || tn == 4);
     else if (tile->kernel == 32)
         built = (tile->waves == 4 || tile->waves == 8) && (tn == 1 || tn == 2) &&

@@ -42,7 +42,7 @@ struct ConvArgs {
     const int8_t *shift;
     const int32_t *thresh; // staircase thresholds [M][2^bits - 1]
     int32_t n, h, w_, pb;  // input size, packed bytes per pixel
-    int32_t c8;            // channels (= bytes of an unpacked int8 pixel)
+    int32_t c8;            // bytes of a staged pixel: channels (int8), or channels / 2 (e2m1)
     int32_t m, kh, kw, sh, sw, ph, pw, ho, wo;
     int32_t wrow;          // packed bytes per filter bank
     int32_t epi, clip_lo, clip_hi, ypb;  // ypb: output bytes per pixel
@@ -107,6 +107,8 @@ hipError_t launch_conv_mfma_b2(const ConvArgs &a, int mr, int nc, int al16, dim3
 hipError_t launch_conv_m32_b8(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_m32_b4(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_m32_b2(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
+// INT-2 through the e2m1 (FP4) matrix instruction
+hipError_t launch_conv_m32_f4(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s);
 hipError_t launch_maxpool(const PoolArgs &a, int bits, hipStream_t s);
 hipError_t launch_relu_s8(const uint8_t *x, uint8_t *y, size_t count, hipStream_t s);

@@ -25,7 +25,7 @@ def test_exports_every_header_function(q, L):
     assert len(names) >= 12
     for name in names:
         assert hasattr(L, name), name
-    assert L.qnn_abi_version() == 4
+    assert L.qnn_abi_version() == 5
 
 
 def test_status_strings(q, L):
@@ -239,3 +239,25 @@ def test_host_pack_rejects_out_of_range(q, L):
                            out.ctypes.data_as(ctypes.c_void_p)) == 4
     assert L.qnn_pack_host(codes.ctypes.data_as(ctypes.c_void_p), 2, 3,
                            out.ctypes.data_as(ctypes.c_void_p)) == 2
+
+
+def test_conv_fp4_validation(q, L):
+    """The e2m1 (FP4) path: INT-2 only, built tile shapes or (0, 0, 0) for the
+    library's pick, filter volume bounded by the exact fp32 range."""
+    g = (3, 3, 1, 1, 1, 1)
+    REQ2 = (0, None, FAKE, FAKE, None, 0, 3)
+    args = ((1, 8, 8, 64), 2, 64, g, REQ2, (1, 8, 8, 64, 2))
+    fp4 = q.TILE_FP4
+    for tile in [(fp4, 0, 0, 0), (fp4, 1, 1, 4), (fp4, 2, 2, 4), (fp4, 2, 1, 8), (fp4, 2, 2, 8)]:
+        assert call_conv_tiled(q, L, *args, tile) == 8, tile      # valid: no GPU here
+    for tile in [(fp4, 4, 1, 4), (fp4, 1, 4, 4), (fp4, 0, 1, 0), (fp4, 1, 1, 2), (fp4, 1, 1, 0)]:
+        assert call_conv_tiled(q, L, *args, tile) == 4, tile      # shapes that are not built
+    # 8- and 4-bit layers have no e2m1 form
+    assert call_conv_tiled(q, L, (1, 8, 8, 32), 8, 64, g, REQ8, (1, 8, 8, 64, 8), (fp4, 0, 0, 0)) == 2
+    assert call_conv_tiled(q, L, (1, 8, 8, 64), 4, 64, g, (0, None, FAKE, FAKE, None, 0, 15),
+                           (1, 8, 8, 64, 4), (fp4, 1, 1, 4)) == 2
+    # eight waves need whole 16-byte chunks of e2m1 pixels: 32 channels
+    assert call_conv_tiled(q, L, (1, 8, 8, 16), 2, 64, g, REQ2, (1, 8, 8, 64, 2), (fp4, 1, 1, 8)) == 4
+    # 9 * 310720 = 2796480 > 2^24 / 6: partial sums could leave the exact fp32 range
+    big = ((1, 3, 3, 310720), 2, 32, g, REQ2, (1, 3, 3, 32, 2))
+    assert call_conv_tiled(q, L, *big, (fp4, 0, 0, 0)) == 6

@@ -1,0 +1,119 @@
+"""GPU parity of the INT-2 path on the FP4 (e2m1) matrix instruction
+(qnn_conv2d_tiled with QNN_TILE_FP4) against the CPU oracle, byte for byte:
+random small layers of every geometry class and epilogue, every FP4 tile
+shape, accumulators at the extremes of the code ranges, and the batch-256
+16x16x128 layer on sampled images."""
+import numpy as np
+import pytest
+
+import synth
+from gpu_helpers import dev, log, oracle_conv, sample_images, with_epi
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def qnn():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1908_11263_amd as q
+    q.device_check()
+    return q
+
+
+def fp4_tiles(q):
+    return [(q.TILE_FP4, 0, 0, 0)] + [(q.TILE_FP4, m, n, w) for m in (1, 2) for n in (1, 2)
+                                      for w in (4, 8)]
+
+
+def run_fp4(qnn, L, tile=None, epi=None):
+    import torch
+    epi = epi or L.epi
+    tile = tile or (qnn.TILE_FP4, 0, 0, 0)
+    y = qnn.conv2d(dev(L.x), (L.n, L.h, L.w, L.c), L.bits, dev(L.wt), L.m, L.kh, L.kw, L.stride,
+                   L.pad, epi, bias=dev(L.bias), mult=dev(L.mult), shift=dev(L.shift),
+                   thresh=dev(L.thresh), clip=L.clip, tile=tile)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+def check(qnn, orc, L, tile=None, epi=None, images=None):
+    epi = epi or L.epi
+    log("case fp4", L.name, epi, "tile", tile, "N=%d H=%d W=%d C=%d M=%d k=%dx%d s=%s p=%s" % (
+        L.n, L.h, L.w, L.c, L.m, L.kh, L.kw, L.stride, L.pad))
+    got = run_fp4(qnn, L, tile, epi)
+    want = oracle_conv(orc, L, epi, images)
+    if images is not None:
+        got = got[images]
+    bad = np.argwhere(got != want)
+    assert bad.size == 0, "%s tile %s: %d mismatches, first at %s" % (
+        L.name, tile, len(bad), bad[:5].tolist())
+    return got
+
+
+@pytest.mark.parametrize("epi", ["requant", "raw32", "stair"])
+def test_fp4_random_layers(qnn, orc, epi):
+    """16, 32 and 48 channels (row walk, tap walk), strides 1-2, pads 0-2,
+    kernels 1-5, 1-40 filters."""
+    rng = np.random.default_rng({"requant": 41, "raw32": 42, "stair": 43}[epi])
+    for _ in range(16):
+        check(qnn, orc, synth.random_small_layer(rng, 2, epi=epi))
+
+
+def layer(n, h, w, c, m, k, seed, epi="requant"):
+    return synth.conv_layer("fp4_int2", 2, n, h, w, c, m, k, k // 2, seed, (0, 3), (-2, 1),
+                            bias_rng=(-150, 150), mult_rng=(1, 1 << 10), shift=10, clip=(0, 3),
+                            epi=epi, thresh_rng=(-k * k * c // 2, k * k * c // 2))
+
+
+def test_fp4_every_tile_shape(qnn, orc):
+    for L in (layer(3, 13, 17, 64, 70, 3, seed=7), layer(2, 9, 6, 16, 33, 1, seed=8),
+              layer(2, 11, 10, 32, 40, 3, seed=9, epi="stair")):
+        want = oracle_conv(orc, L)
+        for tile in fp4_tiles(qnn):
+            log("case fp4", L.name, L.epi, "tile", tile, "C=%d M=%d" % (L.c, L.m))
+            if tile[3] == 8 and (L.c % 32 or L.epi == "stair"):
+                # eight waves: whole 16-byte e2m1 chunks per tap, plain epilogues
+                with pytest.raises(qnn.QnnError) as e:
+                    run_fp4(qnn, L, tile)
+                assert e.value.status == 4
+                continue
+            got = run_fp4(qnn, L, tile)
+            bad = np.argwhere(got != want)
+            assert bad.size == 0, "tile %s: %d mismatches, first at %s" % (tile, len(bad), bad[:5].tolist())
+
+
+def test_fp4_extreme_accumulators(qnn, orc):
+    """Every product at its largest magnitude (x = 3 with w = -2, and with
+    w = 1) over the deepest filter that fits: raw sums checked exactly."""
+    for wv in (-2, 1):
+        L = layer(2, 6, 7, 512, 64, 3, seed=11, epi="raw32")
+        x_vals = np.full_like(L.x_vals, 3)
+        w_vals = np.full_like(L.w_vals, wv)
+        E = synth.ConvLayer("fp4_extreme_w%d" % wv, 2, L.n, L.h, L.w, L.c, L.m, L.kh, L.kw,
+                            L.stride, L.pad, "raw32", x_vals, w_vals, L.bias, None, None, None,
+                            (0, 0))
+        got = check(qnn, orc, E)
+        # interior pixels see all 9 taps: 9 * 512 * 3 * w + bias
+        inner = got[:, 1:-1, 1:-1, :]
+        assert np.array_equal(inner, np.broadcast_to(9 * 512 * 3 * wv + L.bias, inner.shape))
+
+
+def test_fp4_int2_layer_batch256(qnn, orc):
+    L = synth.int2_layer()
+    check(qnn, orc, L, images=sample_images(L.n, seed=4))
+    check(qnn, orc, with_epi(L, "raw32"), images=sample_images(L.n, seed=5))
+    check(qnn, orc, synth.centred(L), images=sample_images(L.n, seed=6))
+
+
+def test_fp4_equals_int8_path_full_output(qnn):
+    """The whole batch-256 output of the two INT-2 paths is identical (both
+    are exact; the oracle checks sampled images above)."""
+    import torch
+    L = synth.int2_layer()
+    a = run_fp4(qnn, L)
+    b = qnn.conv2d(dev(L.x), (L.n, L.h, L.w, L.c), 2, dev(L.wt), L.m, 3, 3, L.stride, L.pad,
+                   L.epi, bias=dev(L.bias), mult=dev(L.mult), shift=dev(L.shift), clip=L.clip)
+    torch.cuda.synchronize()
+    assert np.array_equal(a, b.cpu().numpy())
