@@ -8,7 +8,8 @@ layer (one launch of the fused conv + requantize + pack kernel) over the
 batch, inputs resident in device memory.  Steps are captured in a HIP graph
 and replayed; the timed region is bracketed by HIP events recorded on the
 stream the kernels run on.  The other workloads (INT-8 batch 1, INT-2 batch
-256 on the int8 and on the FP4 matrix path, INT-1 batch 1024, the INT-4
+256 on the int8 and on the FP4 matrix path, INT-1 batch 1024 on the XNOR
+and on the FP4 matrix path, the INT-4
 layer with the staircase epilogue, the CIFAR-shaped network at INT-8 and
 INT-4, batch 4096) are reported under "layers".  The CPU oracle is timed on the host on
 the same INT-4 workload for the "cpu_baseline" object.
@@ -26,6 +27,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 PEAK_INT8_TOPS = 5000.0        # MI355X dense int8 matrix-core peak, 10^12 int ops/s
+PEAK_FP4_TFLOPS = 10100.0      # MI355X dense FP4 (e2m1) matrix-core peak, 10^12 flop/s
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E, GB/s
 VALU_LANE_OPS = 256 * 64 * 2.4e9   # 32-bit vector lane-ops/s: 256 CUs x 64 lanes x 2.4 GHz
 XNOR_PEAK_BMACS = VALU_LANE_OPS * 16  # 2 lane-ops (xnor, bcnt) per 32 binary MACs
@@ -306,7 +308,7 @@ def main():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--only", default=None,
-                    help="run only this workload (int8, int4, int2, int2_fp4, int1, int4_stair, cifar8, cifar4)")
+                    help="run only this workload (int8, int4, int2, int2_fp4, int1, int1_fp4, int4_stair, cifar8, cifar4)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-graph", action="store_true", help="launch every step from Python")
     ap.add_argument("--tile-sweep", action="store_true",
@@ -344,6 +346,7 @@ def main():
         "int2": lambda: ConvStep(synth.int2_layer()),
         "int2_fp4": lambda: ConvStep(synth.int2_layer(), tile=(TILE_FP4, 0, 0, 0)),
         "int1": lambda: ConvStep(synth.int1_layer()),
+        "int1_fp4": lambda: ConvStep(synth.int1_layer(), tile=(TILE_FP4, 0, 0, 0)),
         "int4_stair": lambda: ConvStep(synth.int4_stair_layer()),
         "cifar8": lambda: NetworkStep(synth.cifar_network(8, n=4096)),
         "cifar4": lambda: NetworkStep(synth.cifar_network(4, n=4096)),
@@ -362,6 +365,10 @@ def main():
         rec = {"macs_per_step": step.macs, "us_per_step": round(sec * 1e6, 3), "steps": done,
                "gmacs": round(gmacs, 2),
                "pct_int8_mfma_peak": round(100 * 2 * step.macs / sec / 1e12 / PEAK_INT8_TOPS, 3)}
+        if name == "int2_fp4":
+            rec["pct_fp4_mfma_peak"] = round(100 * 2 * step.macs / sec / 1e12 / PEAK_FP4_TFLOPS, 3)
+        if name == "int1_fp4":
+            rec["pct_fp4_mfma_peak"] = round(100 * 2 * step.macs / sec / 1e12 / PEAK_FP4_TFLOPS, 3)
         if name == "int1":
             rec["pct_xnor_valu_roofline"] = round(100 * step.macs / sec / XNOR_PEAK_BMACS, 3)
         if "cifar" in name:

@@ -115,12 +115,14 @@ typedef struct {
 /* qnn_tile.kernel values. */
 #define QNN_TILE_MFMA16 16 /* v_mfma_i32_16x16x64_i8 */
 #define QNN_TILE_MFMA32 32 /* v_mfma_i32_32x32x32_i8 */
-/* INT-2 layers only: v_mfma_scale_f32_32x32x64_f8f6f4 on FP4 (e2m1) operands.
- * Every INT-2 code is an exact e2m1 value (activations x as x/2, weights w as
- * w/2, products rescaled by a block exponent of 2) and every partial sum is an
- * integer below 2^24, so the fp32 accumulator and hence the output equal the
- * int8 path's bit for bit, at twice the matrix-core rate per instruction.
- * The library never picks it by itself. */
+/* INT-2 and INT-1 layers: v_mfma_scale_f32_32x32x64_f8f6f4 on FP4 (e2m1)
+ * operands.  Every INT-2 code is an exact e2m1 value (activations x as x/2,
+ * weights w as w/2, products rescaled by a block exponent of 2), so is every
+ * INT-1 value (+1, -1), and every partial sum is an integer below 2^24, so
+ * the fp32 accumulator and hence the output equal the integer paths' bit for
+ * bit, at twice the int8 matrix-core rate per instruction.  INT-1 layers take
+ * QNN_EPI_THRESH1 or QNN_EPI_RAW32 as on the XNOR path.  The library never
+ * picks this path by itself. */
 #define QNN_TILE_FP4 4
 
 /* Tile shape of the matrix-core convolution kernels, for exploration and
@@ -187,8 +189,9 @@ qnn_status qnn_linear(const qnn_tensor *x, const void *x_dev, int32_t m, const v
  * paper's study of register-blocked kernel sizes, Sec. IV-C / Fig. 9) or
  * matrix instruction (QNN_TILE_FP4: the sub-byte SIMD the paper's outlook in
  * Sec. VI asks for, on MI355X's FP4 matrix cores): identical results,
- * different speed.  8-, 4- and 2-bit inputs (QNN_TILE_FP4: 2-bit only, else
- * QNN_ERR_BITS; filter volume kh*kw*C above 2796202 QNN_ERR_OVERFLOW);
+ * different speed.  8-, 4- and 2-bit inputs (QNN_TILE_FP4: 2- and 1-bit only,
+ * else QNN_ERR_BITS; filter volume kh*kw*C above 2796202 at 2 bits or 2^24
+ * at 1 bit QNN_ERR_OVERFLOW; other tiles at 1 bit: QNN_ERR_PARAM);
  * shapes that are not built return QNN_ERR_PARAM, tiles that do not fit the
  * local memory (or a single-tile eight-wave plan that the device cannot
  * hold) QNN_ERR_UNSUPPORTED.

@@ -1,5 +1,5 @@
-// INT-2 convolution on the e2m1 (FP4) matrix instruction: instantiations of
-// the 32x32 implicit-GEMM kernel in FP4 mode.
+// INT-2 and INT-1 convolution on the e2m1 (FP4) matrix instruction:
+// instantiations of the 32x32 implicit-GEMM kernel in FP4 mode.
 #include "conv_m32_impl.h"
 
 namespace qnn {

@@ -41,21 +41,43 @@ template <bool F4> struct AccTile { typedef v16i type; };
 template <> struct AccTile<true> { typedef v16f type; };
 
 // One 32x32x64 e2m1 MFMA: rows = A (16 bytes per lane, 32 codes), columns =
-// B; the exponent-2 scale on A restores the factor 1/4 of the x/2, w/2
-// encoding (E8M0 scale bytes: 127 + 2 and 127 + 0).
+// B.  At 2 bits the exponent-2 scale on A restores the factor 1/4 of the
+// x/2, w/2 encoding; 1-bit values (+1, -1) are encoded as they are (E8M0
+// scale bytes: 127 + 2 or 127, and 127 on B).
+template <int BITS>
 __device__ __forceinline__ v16f mfma_f4(v4i a, v4i b, v16f c)
 {
     const v8i a8 = {a.x, a.y, a.z, a.w, 0, 0, 0, 0};
     const v8i b8 = {b.x, b.y, b.z, b.w, 0, 0, 0, 0};
-    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, 129, 0, 127);
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a8, b8, c, 4, 4, 0, BITS == 1 ? 127 : 129,
+                                                           0, 127);
 }
 
-// 16 packed INT-2 weight bytes (64 codes) -> 32 bytes of e2m1 nibbles.
+// 16 packed INT-2 / INT-1 weight bytes (64 / 128 codes) -> 32 / 64 bytes of
+// e2m1 nibbles.
+template <int BITS>
 __device__ __forceinline__ void store_w16_f4(uint8_t *dst, uint4 v)
 {
-    const uint2 a = w2_word_f4(v.x), b = w2_word_f4(v.y), c = w2_word_f4(v.z), d = w2_word_f4(v.w);
-    *(uint4 *)dst = make_uint4(a.x, a.y, b.x, b.y);
-    *(uint4 *)(dst + 16) = make_uint4(c.x, c.y, d.x, d.y);
+    if (BITS == 1) {
+        *(uint4 *)dst = b1_word_f4(v.x);
+        *(uint4 *)(dst + 16) = b1_word_f4(v.y);
+        *(uint4 *)(dst + 32) = b1_word_f4(v.z);
+        *(uint4 *)(dst + 48) = b1_word_f4(v.w);
+    } else {
+        const uint2 a = w2_word_f4(v.x), b = w2_word_f4(v.y), c = w2_word_f4(v.z), d = w2_word_f4(v.w);
+        *(uint4 *)dst = make_uint4(a.x, a.y, b.x, b.y);
+        *(uint4 *)(dst + 16) = make_uint4(c.x, c.y, d.x, d.y);
+    }
+}
+
+// One packed 4-byte weight word in FP4 mode: 8 (INT-2) or 16 (INT-1) bytes.
+template <int BITS>
+__device__ __forceinline__ void store_w4_f4(uint8_t *dst, uint32_t v)
+{
+    if (BITS == 1)
+        *(uint4 *)dst = b1_word_f4(v);
+    else
+        *(uint2 *)dst = w2_word_f4(v);
 }
 
 template <int BITS>
@@ -103,6 +125,18 @@ __device__ __forceinline__ uint32_t pack_codes_word(const uint8_t *src)
         const uint2 v = *(const uint2 *)src;
         const uint32_t x = v.x | (v.x >> 4), y = v.y | (v.y >> 4);
         return __builtin_amdgcn_perm(y, x, 0x06040200u);
+    } else if (BITS == 1) {
+        // 32 bytes of 0 / 1: per word, bits 0..3 of t | t >> 14 (t = v | v >> 7)
+        // are its 4 codes
+        const uint4 a = *(const uint4 *)src, b = *(const uint4 *)(src + 16);
+        const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+        uint32_t r = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t t = w[i] | (w[i] >> 7);
+            r |= ((t | (t >> 14)) & 15u) << (4 * i);
+        }
+        return r;
     } else {
         // byte 0 of u = v | v >> 6, then u | u >> 12, holds channels 0..3
         const uint4 v = *(const uint4 *)src;
@@ -168,6 +202,12 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
     // LDS bytes of one K chunk of a filter row: packed codes (16 K values),
     // or 16 bytes of e2m1 nibbles (32 K values) in FP4 mode
     constexpr int CB = F4 ? 16 : 2 * BITS;
+    // FP4 mode: staged bytes per packed byte (2 at 2 bits, 4 at 1 bit)
+    constexpr int XR = F4 ? 4 / BITS : 1;
+    // threshold epilogues (the staircase, and the binary threshold as a
+    // one-step staircase) are compiled into the extended instances and into
+    // every 1-bit one
+    constexpr bool THR = EXT || BITS == 1;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wv = tid >> 6;
@@ -234,7 +274,7 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
     constexpr int NTH = BITS == 8 ? 1 : (1 << BITS) - 1;  // staircase thresholds per channel
     auto make_plans = [&](const int32_t *wsum) {
         int mode = 0;
-        if (EXT && has_ch && a.epi == EPI_STAIR) {
+        if (THR && has_ch && (a.epi == EPI_STAIR || a.epi == EPI_THRESH1)) {
             const bool live = m0 + pch < a.m;
             stair_thresholds(live ? a.thresh + (size_t)(m0 + pch) * NTH : nullptr, NTH, p_bias, SL,
                              (int32_t *)(sEpi + 4 * pch));
@@ -298,7 +338,7 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
             if (idx < nq) {
                 const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
                 if (F4)
-                    store_w16_f4(sW + row * a.kp + (idx - row * qrow) * 32, wq[u]);
+                    store_w16_f4<BITS>(sW + row * a.kp + (idx - row * qrow) * 16 * XR, wq[u]);
                 else
                     store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
             }
@@ -317,7 +357,7 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 if (idx < nq) {
                     const int row = (int)fdiv((uint32_t)idx, a.div_qrow);
                     if (F4)
-                        store_w16_f4(sW + row * a.kp + (idx - row * qrow) * 32, wq[u]);
+                        store_w16_f4<BITS>(sW + row * a.kp + (idx - row * qrow) * 16 * XR, wq[u]);
                     else
                         store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
                 }
@@ -331,13 +371,14 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
         }
     } else {
         // general order (row walk for small C): one packed 4-byte word per
-        // item, staged as IB bytes (itself, or 8 bytes of e2m1 nibbles)
-        constexpr int IB = F4 ? 8 : 4;
+        // item, staged as IB bytes (itself, or 8 / 16 bytes of e2m1 nibbles)
+        constexpr int IB = 4 * XR;
         const int wpr = kch * CB / IB;  // items per staged row
         const int nit = MT * wpr;
         constexpr int U = 4;
         for (int b0 = tid; b0 < nit; b0 += NT * U) {
             uint32_t v[U];
+            bool ok[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int idx = b0 + u * NT;
@@ -346,10 +387,11 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 const int j = col / (CB / IB), d = col - j * (CB / IB);
                 const int mg = m0 + row;
                 // the chunk's packed offset in the filter row and its real bytes
-                const int pnat = F4 ? sNat[j] / 2 : sNat[j] * BITS / 8;
-                const int pvld = F4 ? sVld[j] / 2 : sVld[j] * BITS / 8;
+                const int pnat = F4 ? sNat[j] / XR : sNat[j] * BITS / 8;
+                const int pvld = F4 ? sVld[j] / XR : sVld[j] * BITS / 8;
                 v[u] = 0;
-                if (idx < nit && mg < a.m && 4 * d < pvld)
+                ok[u] = idx < nit && mg < a.m && 4 * d < pvld;
+                if (ok[u])
                     v[u] = *(const uint32_t *)(a.w + (size_t)mg * a.wrow + pnat + 4 * d);
             }
 #pragma unroll
@@ -357,10 +399,15 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 const int idx = b0 + u * NT;
                 if (idx < nit) {
                     const int row = (int)fdiv((uint32_t)idx, a.div_ncol);
-                    if (F4)
-                        *(uint2 *)(sW + row * a.kp + 8 * (idx - row * wpr)) = w2_word_f4(v[u]);
+                    uint8_t *dst = sW + row * a.kp + IB * (idx - row * wpr);
+                    if (!F4)
+                        *(uint32_t *)dst = v[u];
+                    else if (ok[u])
+                        store_w4_f4<BITS>(dst, v[u]);
+                    else if (BITS == 1)
+                        *(uint4 *)dst = make_uint4(0, 0, 0, 0);  // K padding: e2m1 zeros
                     else
-                        *(uint32_t *)(sW + row * a.kp + 4 * (idx - row * wpr)) = v[u];
+                        *(uint2 *)dst = make_uint2(0, 0);
                 }
             }
         }
@@ -487,7 +534,7 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
 #pragma unroll
                 for (int c = 0; c < WN; ++c) {
                     if constexpr (F4)
-                        acc[t][c] = mfma_f4(B[c], av, acc[t][c]);
+                        acc[t][c] = mfma_f4<BITS>(B[c], av, acc[t][c]);
                     else
                         acc[t][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(B[c], av, acc[t][c], 0, 0, 0);
                 }
@@ -578,16 +625,21 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
 #pragma unroll
             for (int t = 0; t < WM; ++t) {
                 const int ch = t * 32 + r32;
-                if (EXT && BITS != 8 && a.epi == EPI_STAIR) {
-                    // staircase (Eq. (4)): count the channel's thresholds at or below acc'
+                if (THR && BITS != 8 && (a.epi == EPI_STAIR || a.epi == EPI_THRESH1)) {
+                    // staircase (Eq. (4)): count the channel's thresholds at or below
+                    // acc' (one threshold: the binary output of Eq. (5))
                     int32_t T[16];
+                    if (NTH == 1) {
+                        T[0] = ((const int32_t *)(sEpi + 4 * ch))[0];
+                    } else {
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        const int4 q4 = sEpi[4 * ch + k];
-                        T[4 * k] = q4.x;
-                        T[4 * k + 1] = q4.y;
-                        T[4 * k + 2] = q4.z;
-                        T[4 * k + 3] = q4.w;
+                        for (int k = 0; k < 4; ++k) {
+                            const int4 q4 = sEpi[4 * ch + k];
+                            T[4 * k] = q4.x;
+                            T[4 * k + 1] = q4.y;
+                            T[4 * k + 2] = q4.z;
+                            T[4 * k + 3] = q4.w;
+                        }
                     }
 #pragma unroll
                     for (int c = 0; c < WN; ++c) {

@@ -86,6 +86,16 @@ __device__ __forceinline__ uint2 w2_word_f4(uint32_t v)
     return make_uint2(w2_nibbles_f4(t.x), w2_nibbles_f4(t.y));
 }
 
+// INT-1 codes (value 2*bit - 1 for weights and activations alike) as e2m1
+// +1.0 (0010) and -1.0 (1010): one packed word (32 codes) -> 16 bytes, word
+// j of the result holding codes j, j+4, .., j+28 in its nibbles 0..7.
+__device__ __forceinline__ uint4 b1_word_f4(uint32_t v)
+{
+    const uint32_t m = 0x11111111u, neg = 0xAAAAAAAAu;
+    return make_uint4(neg ^ ((v & m) << 3), neg ^ (((v >> 1) & m) << 3), neg ^ (((v >> 2) & m) << 3),
+                      neg ^ (((v >> 3) & m) << 3));
+}
+
 // Weights, one packed word -> 8 (INT-4) or 16 (INT-2) bytes holding 16*w /
 // 64*w: the code moved to the top of its byte is exactly that signed byte.
 __device__ __forceinline__ uint2 w4_word(uint32_t v)
@@ -282,6 +292,15 @@ __device__ __forceinline__ void halo_store(uint8_t *sX, const uint4 *v, const in
     for (int u = 0; u < U; ++u) {
         if (dst[u] >= 0) {
             uint8_t *d = sX + dst[u];
+            if (F4 && BITS == 1) {
+                *(uint4 *)d = b1_word_f4(v[u].x);
+                if (Q16) {
+                    *(uint4 *)(d + 16) = b1_word_f4(v[u].y);
+                    *(uint4 *)(d + 32) = b1_word_f4(v[u].z);
+                    *(uint4 *)(d + 48) = b1_word_f4(v[u].w);
+                }
+                continue;
+            }
             if (F4) {
                 const uint2 p = x2_word_f4(v[u].x);
                 if (Q16) {

@@ -420,11 +420,11 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     const int64_t K = (int64_t)g->kh * g->kw * x->c;
     if (K > max_k_for(x->bits))
         return QNN_ERR_OVERFLOW;
-    // the e2m1 path: INT-2 codes staged as nibbles, half a byte per channel;
-    // its fp32 accumulation is exact while every partial sum stays below 2^24
-    // in magnitude (|x * w| <= 3 * 2 per term)
+    // the e2m1 path: INT-2 / INT-1 codes staged as nibbles, half a byte per
+    // channel; its fp32 accumulation is exact while every partial sum stays
+    // below 2^24 in magnitude (|x * w| <= 3 * 2, or 1, per term)
     const bool f4 = force && force->kernel == QNN_TILE_FP4;
-    if (f4 && K * 6 > ((int64_t)1 << 24))
+    if (f4 && K * (x->bits == 1 ? 1 : 6) > ((int64_t)1 << 24))
         return QNN_ERR_OVERFLOW;
     if ((int64_t)x->n * ho * wo >= ((int64_t)1 << 31) || (int64_t)x->n * x->h * x->w >= ((int64_t)1 << 31))
         return QNN_ERR_SHAPE;
@@ -438,7 +438,7 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     const int ypb = (int)pixel_bytes64(y);
     int cus = 0;
 
-    if (x->bits == 1) {
+    if (x->bits == 1 && !f4) {
         st = device_info(&cus);
         if (st != QNN_OK)
             return st;
@@ -563,7 +563,7 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     a.div_ptw = make_fastdiv((uint32_t)(a.tw / 2 > 0 ? a.tw / 2 : 1));
     // staging items per filter row: int8 words (16x16 kernel), packed words,
     // or 8-byte e2m1 groups (one packed word each)
-    a.div_ncol = make_fastdiv((uint32_t)(f4 ? 2 * a.kch : (use32 ? a.kch * x->bits / 2 : 4 * a.kch)));
+    a.div_ncol = make_fastdiv((uint32_t)(f4 ? a.kch * x->bits : (use32 ? a.kch * x->bits / 2 : 4 * a.kch)));
     const int mtiles = (m + MT - 1) / MT;
     const int per_cu = (a.lds_bytes * 2 <= kLdsBytes && nw == 4) ? 2 : 1;
     int64_t gx = (int64_t)cus * per_cu;
@@ -574,7 +574,8 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     dim3 grid((unsigned)gx, (unsigned)mtiles);
     hipError_t err;
     if (f4) {
-        err = launch_conv_m32_f4(a, wm, wn, al16, nw, grid, s);
+        err = x->bits == 1 ? launch_conv_m32_f4b1(a, wm, wn, al16, nw, grid, s)
+                           : launch_conv_m32_f4(a, wm, wn, al16, nw, grid, s);
     } else if (use32) {
         if (x->bits == 8)
             err = launch_conv_m32_b8(a, wm, wn, al16, nw, grid, s);
@@ -673,12 +674,12 @@ qnn_status qnn_conv2d_tiled(const qnn_tensor *x, const void *x_dev, int32_t m, c
 {
     if (!tile)
         return QNN_ERR_NULL;
-    if (x && x->bits == 1)
-        return QNN_ERR_PARAM;  // the binary kernel has no matrix tiles
+    if (x && x->bits == 1 && tile->kernel != QNN_TILE_FP4)
+        return QNN_ERR_PARAM;  // the XNOR kernel has no matrix tiles
     const int tm = tile->tile_m, tn = tile->tile_n;
     bool built = false;
     if (tile->kernel == QNN_TILE_FP4) {
-        if (x && x->bits != 2)
+        if (x && x->bits != 2 && x->bits != 1)
             return QNN_ERR_BITS;
         built = (tm == 0 && tn == 0 && tile->waves == 0) ||
                 ((tile->waves == 4 || tile->waves == 8) && (tn == 1 || tn == 2) && (tm == 1 || tm == 2));

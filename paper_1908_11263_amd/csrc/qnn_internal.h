@@ -107,8 +107,9 @@ hipError_t launch_conv_mfma_b2(const ConvArgs &a, int mr, int nc, int al16, dim3
 hipError_t launch_conv_m32_b8(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_m32_b4(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_m32_b2(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
-// INT-2 through the e2m1 (FP4) matrix instruction
+// INT-2 and INT-1 through the e2m1 (FP4) matrix instruction
 hipError_t launch_conv_m32_f4(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
+hipError_t launch_conv_m32_f4b1(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s);
 hipError_t launch_maxpool(const PoolArgs &a, int bits, hipStream_t s);
 hipError_t launch_relu_s8(const uint8_t *x, uint8_t *y, size_t count, hipStream_t s);

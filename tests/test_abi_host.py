@@ -252,6 +252,11 @@ def test_conv_fp4_validation(q, L):
         assert call_conv_tiled(q, L, *args, tile) == 8, tile      # valid: no GPU here
     for tile in [(fp4, 4, 1, 4), (fp4, 1, 4, 4), (fp4, 0, 1, 0), (fp4, 1, 1, 2), (fp4, 1, 1, 0)]:
         assert call_conv_tiled(q, L, *args, tile) == 4, tile      # shapes that are not built
+    # 1-bit layers: the e2m1 path only (binary threshold or raw sums)
+    TH1 = (1, None, None, None, FAKE, 0, 0)
+    assert call_conv_tiled(q, L, (1, 8, 8, 64), 1, 64, g, TH1, (1, 8, 8, 64, 1), (fp4, 0, 0, 0)) == 8
+    assert call_conv_tiled(q, L, (1, 8, 8, 64), 1, 64, g, TH1, (1, 8, 8, 64, 1), (fp4, 1, 2, 8)) == 8
+    assert call_conv_tiled(q, L, (1, 8, 8, 64), 1, 64, g, TH1, (1, 8, 8, 64, 1), (32, 1, 1, 4)) == 4
     # 8- and 4-bit layers have no e2m1 form
     assert call_conv_tiled(q, L, (1, 8, 8, 32), 8, 64, g, REQ8, (1, 8, 8, 64, 8), (fp4, 0, 0, 0)) == 2
     assert call_conv_tiled(q, L, (1, 8, 8, 64), 4, 64, g, (0, None, FAKE, FAKE, None, 0, 15),

@@ -1,8 +1,9 @@
-"""GPU parity of the INT-2 path on the FP4 (e2m1) matrix instruction
-(qnn_conv2d_tiled with QNN_TILE_FP4) against the CPU oracle, byte for byte:
-random small layers of every geometry class and epilogue, every FP4 tile
-shape, accumulators at the extremes of the code ranges, and the batch-256
-16x16x128 layer on sampled images."""
+"""GPU parity of the INT-2 and INT-1 paths on the FP4 (e2m1) matrix
+instruction (qnn_conv2d_tiled with QNN_TILE_FP4) against the CPU oracle,
+byte for byte: random small layers of every geometry class and epilogue,
+every FP4 tile shape, accumulators at the extremes of the code ranges, the
+batch-256 16x16x128 INT-2 layer and the batch-1024 8x8x256 INT-1 layer on
+sampled images, and both whole outputs against the integer paths."""
 import numpy as np
 import pytest
 
@@ -115,5 +116,61 @@ def test_fp4_equals_int8_path_full_output(qnn):
     a = run_fp4(qnn, L)
     b = qnn.conv2d(dev(L.x), (L.n, L.h, L.w, L.c), 2, dev(L.wt), L.m, 3, 3, L.stride, L.pad,
                    L.epi, bias=dev(L.bias), mult=dev(L.mult), shift=dev(L.shift), clip=L.clip)
+    torch.cuda.synchronize()
+    assert np.array_equal(a, b.cpu().numpy())
+
+
+# ------------------------------------------------------------------ INT-1
+
+@pytest.mark.parametrize("epi", ["thresh1", "raw32"])
+def test_fp4_int1_random_layers(qnn, orc, epi):
+    """32, 64 and 96 channels, strides 1-2, pads 0-2 (padding taps are -1),
+    kernels 1-5, 1-79 filters."""
+    rng = np.random.default_rng({"thresh1": 51, "raw32": 52}[epi])
+    for _ in range(16):
+        check(qnn, orc, synth.random_small_layer(rng, 1, epi=epi))
+
+
+def int1_layer(n, h, w, c, m, k, seed, epi="thresh1"):
+    return synth.conv_layer("fp4_int1", 1, n, h, w, c, m, k, k // 2, seed, None, None,
+                            bias_rng=(-20, 20), thresh_rng=(-k * k * c // 4, k * k * c // 4), epi=epi)
+
+
+def test_fp4_int1_every_tile_shape(qnn, orc):
+    for L in (int1_layer(3, 13, 17, 64, 70, 3, seed=21), int1_layer(2, 9, 6, 32, 33, 1, seed=22),
+              int1_layer(2, 11, 10, 96, 40, 3, seed=23, epi="raw32")):
+        want = oracle_conv(orc, L)
+        for tile in fp4_tiles(qnn):
+            log("case fp4", L.name, L.epi, "tile", tile, "C=%d M=%d" % (L.c, L.m))
+            got = run_fp4(qnn, L, tile)
+            bad = np.argwhere(got != want)
+            assert bad.size == 0, "tile %s: %d mismatches, first at %s" % (tile, len(bad), bad[:5].tolist())
+
+
+def test_fp4_int1_extreme_accumulators(qnn, orc):
+    """All +1 against all -1 and all +1 over a deep filter: raw sums of
+    -K and +K, with the -1 padding taps at the borders."""
+    for wv in (-1, 1):
+        L = int1_layer(2, 6, 7, 512, 64, 3, seed=24, epi="raw32")
+        E = synth.ConvLayer("fp4_int1_extreme_w%d" % wv, 1, L.n, L.h, L.w, L.c, L.m, L.kh, L.kw,
+                            L.stride, L.pad, "raw32", np.ones_like(L.x_vals),
+                            np.full_like(L.w_vals, wv), L.bias, None, None, None, (0, 0))
+        got = check(qnn, orc, E)
+        inner = got[:, 1:-1, 1:-1, :]
+        assert np.array_equal(inner, np.broadcast_to(9 * 512 * wv + L.bias, inner.shape))
+
+
+def test_fp4_int1_layer_batch1024(qnn, orc):
+    L = synth.int1_layer()
+    check(qnn, orc, L, images=sample_images(L.n, seed=7))
+    check(qnn, orc, with_epi(L, "raw32"), images=sample_images(L.n, seed=8))
+
+
+def test_fp4_int1_equals_xnor_path_full_output(qnn):
+    import torch
+    L = synth.int1_layer()
+    a = run_fp4(qnn, L)
+    b = qnn.conv2d(dev(L.x), (L.n, L.h, L.w, L.c), 1, dev(L.wt), L.m, 3, 3, L.stride, L.pad,
+                   L.epi, bias=dev(L.bias), thresh=dev(L.thresh))
     torch.cuda.synchronize()
     assert np.array_equal(a, b.cpu().numpy())
