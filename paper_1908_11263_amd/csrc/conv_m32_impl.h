@@ -224,17 +224,17 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
     uint8_t *sC = smem + a.off_out;                              // [pixel][cs] one byte per code
 
     // ---- prologue: every independent load is issued before any is used ----
-    const int pch = wv + NW * lane;
-    const bool has_ch = lane < MT / NW;
-    int32_t p_bias = 0, p_mult = 0, p_shift = 0;
-    if (has_ch && m0 + pch < a.m) {
-        if (a.bias)
-            p_bias = a.bias[m0 + pch];
-        if (a.epi == EPI_REQUANT) {
-            p_mult = a.mult[m0 + pch];
-            p_shift = a.shift[m0 + pch];
-        }
-    }
+    // the input tile first: its loads are the longest chain of the prologue
+    int tile = blockIdx.x;
+    TileXY T = tile_xy(a, tile < a.ntiles ? tile : 0);
+    constexpr int UH = 4;
+    uint4 hq[UH];
+    int hd[UH];
+    const int totq = a.ti * a.hh * a.hwd * a.pbq;
+    if (a.quad16)
+        halo_issue<BITS, true, UH, NT, F4>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
+    else
+        halo_issue<BITS, false, UH, NT, F4>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
     // filter tile: packed rows m0 .. m0+MT-1 are one contiguous run and, when
     // the K walk is tap by tap, already in chunk order: a plain copy
     const bool wfast = !a.row_mode && (a.wrow & 15) == 0;
@@ -254,16 +254,17 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 wq[u] = wsrc[idx];
         }
     }
-    int tile = blockIdx.x;
-    TileXY T = tile_xy(a, tile < a.ntiles ? tile : 0);
-    constexpr int UH = 4;
-    uint4 hq[UH];
-    int hd[UH];
-    const int totq = a.ti * a.hh * a.hwd * a.pbq;
-    if (a.quad16)
-        halo_issue<BITS, true, UH, NT, F4>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
-    else
-        halo_issue<BITS, false, UH, NT, F4>(a, tid, tile < a.ntiles ? totq : 0, T.n0, T.iy0, T.ix0, hq, hd);
+    const int pch = wv + NW * lane;
+    const bool has_ch = lane < MT / NW;
+    int32_t p_bias = 0, p_mult = 0, p_shift = 0;
+    if (has_ch && m0 + pch < a.m) {
+        if (a.bias)
+            p_bias = a.bias[m0 + pch];
+        if (a.epi == EPI_REQUANT) {
+            p_mult = a.mult[m0 + pch];
+            p_shift = a.shift[m0 + pch];
+        }
+    }
 
     // requantization plans (sub-byte layers: they need no filter sums, so they
     // are computed while the loads above are in flight) and the votes that

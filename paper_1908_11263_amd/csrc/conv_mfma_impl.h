@@ -258,27 +258,30 @@ __device__ __forceinline__ void halo_issue(const ConvArgs &a, int b0, int totq, 
 {
     constexpr int QB = Q16 ? 16 : 4;
     constexpr int QU = QB * (F4 ? 4 : 8) / BITS;
+    const uint8_t *x = a.x;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
         const int idx = b0 + u * NT;
+        const int pix = (int)fdiv((uint32_t)idx, a.div_pbq);
+        const int q = idx - pix * a.pbq;
+        const int hrow = (int)fdiv((uint32_t)pix, a.div_hwd);
+        const int hx = pix - hrow * a.hwd;
+        const int tI = (int)fdiv((uint32_t)hrow, a.div_hh);
+        const int hy = hrow - tI * a.hh;
+        const int nn = n0 + tI, iy = iy0 + hy, ix = ix0 + hx;
+        const bool live = idx < totq;
+        dst[u] = live ? pix * a.ps + q * QU : -1;
+        // one predicate (unsigned compares also reject negative rows and
+        // columns); the input pixel index fits 31 bits (n*h*w < 2^31)
+        const bool ok = live && nn < a.n && (uint32_t)iy < (uint32_t)a.h && (uint32_t)ix < (uint32_t)a.w_;
+        const uint32_t gpix = ((uint32_t)nn * (uint32_t)a.h + (uint32_t)iy) * (uint32_t)a.w_ + (uint32_t)ix;
+        const uint8_t *src = x + (size_t)gpix * (uint32_t)a.pb + q * QB;
         v[u] = make_uint4(0, 0, 0, 0);
-        dst[u] = -1;
-        if (idx < totq) {
-            const int pix = (int)fdiv((uint32_t)idx, a.div_pbq);
-            const int q = idx - pix * a.pbq;
-            const int hrow = (int)fdiv((uint32_t)pix, a.div_hwd);
-            const int hx = pix - hrow * a.hwd;
-            const int tI = (int)fdiv((uint32_t)hrow, a.div_hh);
-            const int hy = hrow - tI * a.hh;
-            const int nn = n0 + tI, iy = iy0 + hy, ix = ix0 + hx;
-            dst[u] = pix * a.ps + q * QU;
-            if (nn < a.n && iy >= 0 && iy < a.h && ix >= 0 && ix < a.w_) {
-                const uint8_t *src = a.x + (((size_t)nn * a.h + iy) * a.w_ + ix) * a.pb + q * QB;
-                if (Q16)
-                    v[u] = *(const uint4 *)src;
-                else
-                    v[u].x = *(const uint32_t *)src;
-            }
+        if (ok) {
+            if (Q16)
+                v[u] = *(const uint4 *)src;
+            else
+                v[u].x = *(const uint32_t *)src;
         }
     }
 }
