@@ -254,8 +254,11 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 wq[u] = wsrc[idx];
         }
     }
-    const int pch = wv + NW * lane;
-    const bool has_ch = lane < MT / NW;
+    // per-channel parameters and plans: computed by (at most) four waves,
+    // one per SIMD, so an eight-wave workgroup pays for them once per SIMD
+    constexpr int PW = NW < 4 ? NW : 4;
+    const int pch = wv + PW * lane;
+    const bool has_ch = wv < PW && lane < MT / PW;
     int32_t p_bias = 0, p_mult = 0, p_shift = 0;
     if (has_ch && m0 + pch < a.m) {
         if (a.bias)
@@ -501,13 +504,9 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 base[c] = ((tI * a.hh + py * a.sh) * a.hwd + px * a.sw) * a.ps;
             }
         }
+        // accumulators: the first K step's MFMAs start from zero
         typedef typename AccTile<F4>::type ACC;
         ACC acc[WM][WN];
-#pragma unroll
-        for (int t = 0; t < WM; ++t)
-#pragma unroll
-            for (int c = 0; c < WN; ++c)
-                acc[t][c] = (ACC){};
         const uint8_t *aRow = sW + r32 * a.kp + h * CB;
         // filter fragments are read in packed form (2 / 1 registers for 4 / 2
         // bits) and expanded right before their MFMAs; two register sets
@@ -528,16 +527,17 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 }
             }
         };
-        auto mfma_step = [&](const PA *A, const v4i *B) {
+        auto mfma_step = [&](const PA *A, const v4i *B, bool zero) {
 #pragma unroll
             for (int t = 0; t < WM; ++t) {
                 const v4i av = expand_a<BITS>(A[t]);
 #pragma unroll
                 for (int c = 0; c < WN; ++c) {
+                    const ACC cin = zero ? (ACC){} : acc[t][c];
                     if constexpr (F4)
-                        acc[t][c] = mfma_f4<BITS>(B[c], av, acc[t][c]);
+                        acc[t][c] = mfma_f4<BITS>(B[c], av, cin);
                     else
-                        acc[t][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(B[c], av, acc[t][c], 0, 0, 0);
+                        acc[t][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(B[c], av, cin, 0, 0, 0);
                 }
             }
         };
@@ -559,15 +559,30 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
             load_frags(1, o.y, a1, b1);
             __builtin_amdgcn_sched_barrier(0);
         }
-        for (int pr = 0; pr < npairs; ++pr) {
-            const int pn = min(pr + 1, npairs - 1);
+        {
+            // the first pair (there is always one), peeled: its first MFMAs
+            // take a zero accumulator instead of zeroed registers
+            const int pn = min(1, npairs - 1);
             const int2 o = tab2[2 * pn];
             __builtin_amdgcn_sched_barrier(0);
-            mfma_step(a0, b0);
+            mfma_step(a0, b0, true);
             __builtin_amdgcn_sched_barrier(0);
             load_frags(2 * pn, o.x, a0, b0);
             __builtin_amdgcn_sched_barrier(0);
-            mfma_step(a1, b1);
+            mfma_step(a1, b1, false);
+            __builtin_amdgcn_sched_barrier(0);
+            load_frags(2 * pn + 1, o.y, a1, b1);
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        for (int pr = 1; pr < npairs; ++pr) {
+            const int pn = min(pr + 1, npairs - 1);
+            const int2 o = tab2[2 * pn];
+            __builtin_amdgcn_sched_barrier(0);
+            mfma_step(a0, b0, false);
+            __builtin_amdgcn_sched_barrier(0);
+            load_frags(2 * pn, o.x, a0, b0);
+            __builtin_amdgcn_sched_barrier(0);
+            mfma_step(a1, b1, false);
             __builtin_amdgcn_sched_barrier(0);
             load_frags(2 * pn + 1, o.y, a1, b1);
             __builtin_amdgcn_sched_barrier(0);
