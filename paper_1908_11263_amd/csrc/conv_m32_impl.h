@@ -193,7 +193,11 @@ __device__ __forceinline__ uint8_t pack_codes_byte(const uint8_t *src)
 // EXT: the staircase epilogue, the fused pooling and the next-tile input
 // prefetch are compiled in; the plain instances (scale-and-clamp and raw
 // layers with one tile per workgroup) carry none of them.
-template <int BITS, int WM, int WN, bool AL16, bool EXT, int NW, bool F4 = false>
+// UA: 4- / 2-bit filters staged in LDS already unpacked to int8 (16*w /
+// 64*w), so the main loop reads 16-byte filter fragments and spends no
+// vector instructions expanding them (instantiated for the eight-wave plain
+// 4-bit tiles).
+template <int BITS, int WM, int WN, bool AL16, bool EXT, int NW, bool F4 = false, bool UA = false>
 __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
 {
     extern __shared__ __align__(16) uint8_t smem[];
@@ -201,9 +205,10 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
     constexpr int MT = 32 * WM;
     // LDS bytes of one K chunk of a filter row: packed codes (16 K values),
     // or 16 bytes of e2m1 nibbles (32 K values) in FP4 mode
-    constexpr int CB = F4 ? 16 : 2 * BITS;
-    // FP4 mode: staged bytes per packed byte (2 at 2 bits, 4 at 1 bit)
-    constexpr int XR = F4 ? 4 / BITS : 1;
+    constexpr int CB = (F4 || UA) ? 16 : 2 * BITS;
+    // staged bytes per packed byte: 2 / 4 at 2 / 1 bits in FP4 mode, 8/BITS
+    // for unpacked filters
+    constexpr int XR = F4 ? 4 / BITS : (UA ? 8 / BITS : 1);
     // threshold epilogues (the staircase, and the binary threshold as a
     // one-step staircase) are compiled into the extended instances and into
     // every 1-bit one
@@ -344,7 +349,10 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 if (F4)
                     store_w16_f4<BITS>(sW + row * a.kp + (idx - row * qrow) * 16 * XR, wq[u]);
                 else
-                    store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
+                    if (UA)
+                        stage_w16<BITS>((int8_t *)(sW + row * a.kp + (idx - row * qrow) * 16 * XR), wq[u]);
+                    else
+                        store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
             }
         }
         for (int b0 = tid + NT * UW; b0 < nq; b0 += NT * UW) {
@@ -363,7 +371,10 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                     if (F4)
                         store_w16_f4<BITS>(sW + row * a.kp + (idx - row * qrow) * 16 * XR, wq[u]);
                     else
-                        store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
+                        if (UA)
+                            stage_w16<BITS>((int8_t *)(sW + row * a.kp + (idx - row * qrow) * 16 * XR), wq[u]);
+                        else
+                            store_packed16<BITS>(sW + row * a.kp + (idx - row * qrow) * 16, wq[u]);
                 }
             }
         }
@@ -404,7 +415,11 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                 if (idx < nit) {
                     const int row = (int)fdiv((uint32_t)idx, a.div_ncol);
                     uint8_t *dst = sW + row * a.kp + IB * (idx - row * wpr);
-                    if (!F4)
+                    if (UA && BITS == 4)
+                        *(uint2 *)dst = w4_word(v[u]);
+                    else if (UA && BITS == 2)
+                        *(uint4 *)dst = w2_word(v[u]);
+                    else if (!F4)
                         *(uint32_t *)dst = v[u];
                     else if (ok[u])
                         store_w4_f4<BITS>(dst, v[u]);
@@ -511,7 +526,7 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
         // filter fragments are read in packed form (2 / 1 registers for 4 / 2
         // bits) and expanded right before their MFMAs; two register sets
         // alternate, so the reads of step k+1 are in flight during step k
-        typedef typename FragA<F4, BITS>::type PA;
+        typedef typename FragA<F4 || UA, BITS>::type PA;
         auto load_frags = [&](int ks, int off, PA *A, v4i *B) {
 #pragma unroll
             for (int t = 0; t < WM; ++t)
@@ -826,7 +841,7 @@ hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, int
 #define QNN_CASE32_X(WM_, WN_, AL_, EXT_, NW_)                                                  \
     if (wm == WM_ && wn == WN_ && al16 == AL_ && ext == EXT_ && nw == NW_) {                    \
         static bool attr_set = false;                                                           \
-        auto *k = conv_m32_kernel<BITS, WM_, WN_, (AL_ != 0), EXT_, NW_, F4>;                   \
+        auto *k = conv_m32_kernel<BITS, WM_, WN_, (AL_ != 0), EXT_, NW_, F4, false>;            \
         if (!attr_set) {                                                                        \
             if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,  \
                                     a.lds_bytes > 64 * 1024 ? 160 * 1024 : 64 * 1024) != hipSuccess) \
@@ -838,6 +853,25 @@ hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, int
     }
 #define QNN_CASE32(WM_, WN_, AL_) QNN_CASE32_X(WM_, WN_, AL_, false, 4) QNN_CASE32_X(WM_, WN_, AL_, true, 4)
     const bool ext = a.pool != 0 || a.epi == EPI_STAIR || (int64_t)grid.x < a.ntiles;
+    if constexpr (!F4 && BITS == 4) {
+        if (a.wunpack && al16 && !ext && nw == 8) {
+#define QNN_CASE32_U(WM_, WN_)                                                                  \
+            if (wm == WM_ && wn == WN_) {                                                       \
+                static bool attr_set = false;                                                   \
+                auto *k = conv_m32_kernel<BITS, WM_, WN_, true, false, 8, false, true>;         \
+                if (!attr_set) {                                                                \
+                    if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, \
+                                            a.lds_bytes > 64 * 1024 ? 160 * 1024 : 64 * 1024) != hipSuccess) \
+                        (void)hipGetLastError();                                                \
+                    attr_set = true;                                                            \
+                }                                                                               \
+                hipLaunchKernelGGL(k, grid, dim3(512), a.lds_bytes, s, a);                      \
+                return hipGetLastError();                                                       \
+            }
+            QNN_CASE32_U(1, 1) QNN_CASE32_U(2, 1) QNN_CASE32_U(1, 2) QNN_CASE32_U(2, 2)
+#undef QNN_CASE32_U
+        }
+    }
     QNN_CASE32(1, 1, 0) QNN_CASE32(1, 2, 0) QNN_CASE32(2, 1, 0) QNN_CASE32(2, 2, 0)
     QNN_CASE32(1, 1, 1) QNN_CASE32(1, 2, 1) QNN_CASE32(2, 1, 1) QNN_CASE32(2, 2, 1)
     // eight-wave workgroups: plain instances for layers with one tile per workgroup

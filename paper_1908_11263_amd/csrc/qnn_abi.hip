@@ -368,9 +368,17 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
             if (allow_nw8 && !a.pool && a.epi != EPI_STAIR && wm <= 2 && al16 &&
                 units <= 2 * kPlanCus) {
                 ConvArgs c8 = b;
-                const int64_t lds8 = fit_tile(c8, MT, 256 * cwn, bits, obits, (int64_t)MT * b.kp, tab_bytes, true);
+                // 4-bit filters staged unpacked (16-byte chunks per row): the
+                // main loop then spends no vector instructions expanding them,
+                // for twice the filter bytes in LDS (measured faster at 4 bits;
+                // at 2 bits the fourfold filter bytes cost more than they save)
+                const bool unpack = !f4 && bits == 4;
+                if (unpack)
+                    c8.kp = (b.kch + 1) * 16;
+                const int64_t lds8 = fit_tile(c8, MT, 256 * cwn, bits, obits, (int64_t)MT * c8.kp, tab_bytes, true);
                 if (lds8 >= 0 && lds8 <= kLdsBytes) {
                     a = c8;
+                    a.wunpack = unpack ? 1 : 0;
                     nw = 8;
                 }
             }

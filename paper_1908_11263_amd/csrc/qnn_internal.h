@@ -75,6 +75,7 @@ struct ConvArgs {
     int32_t pool, hp, wp;
     FastDiv div_ptile;     // (th/2)*(tw/2) pooled pixels per image of a tile
     FastDiv div_ptw;       // tw/2
+    int32_t wunpack;       // 32x32 kernel: 4-/2-bit filters staged unpacked to int8
 };
 
 // Arguments of the INT-1 XNOR/popcount convolution.
