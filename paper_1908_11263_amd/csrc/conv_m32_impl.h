@@ -195,8 +195,8 @@ __device__ __forceinline__ uint8_t pack_codes_byte(const uint8_t *src)
 // layers with one tile per workgroup) carry none of them.
 // UA: 4- / 2-bit filters staged in LDS already unpacked to int8 (16*w /
 // 64*w), so the main loop reads 16-byte filter fragments and spends no
-// vector instructions expanding them (instantiated for the eight-wave plain
-// 4-bit tiles).
+// vector instructions expanding them (instantiated for 4-bit layers walked
+// tap by tap).
 template <int BITS, int WM, int WN, bool AL16, bool EXT, int NW, bool F4 = false, bool UA = false>
 __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
 {
@@ -838,10 +838,10 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
 template <int BITS, bool F4 = false>
 hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s)
 {
-#define QNN_CASE32_X(WM_, WN_, AL_, EXT_, NW_)                                                  \
-    if (wm == WM_ && wn == WN_ && al16 == AL_ && ext == EXT_ && nw == NW_) {                    \
+#define QNN_CASE32_XU(WM_, WN_, AL_, EXT_, NW_, UA_)                                            \
+    if (wm == WM_ && wn == WN_ && al16 == AL_ && ext == EXT_ && nw == NW_ && ua == UA_) {       \
         static bool attr_set = false;                                                           \
-        auto *k = conv_m32_kernel<BITS, WM_, WN_, (AL_ != 0), EXT_, NW_, F4, false>;            \
+        auto *k = conv_m32_kernel<BITS, WM_, WN_, (AL_ != 0), EXT_, NW_, F4, UA_>;              \
         if (!attr_set) {                                                                        \
             if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,  \
                                     a.lds_bytes > 64 * 1024 ? 160 * 1024 : 64 * 1024) != hipSuccess) \
@@ -851,26 +851,17 @@ hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, int
         hipLaunchKernelGGL(k, grid, dim3(64 * NW_), a.lds_bytes, s, a);                         \
         return hipGetLastError();                                                               \
     }
+#define QNN_CASE32_X(WM_, WN_, AL_, EXT_, NW_) QNN_CASE32_XU(WM_, WN_, AL_, EXT_, NW_, false)
 #define QNN_CASE32(WM_, WN_, AL_) QNN_CASE32_X(WM_, WN_, AL_, false, 4) QNN_CASE32_X(WM_, WN_, AL_, true, 4)
     const bool ext = a.pool != 0 || a.epi == EPI_STAIR || (int64_t)grid.x < a.ntiles;
+    const bool ua = a.wunpack != 0;
     if constexpr (!F4 && BITS == 4) {
-        if (a.wunpack && al16 && !ext && nw == 8) {
+        // filters staged unpacked (4-bit layers walked tap by tap)
 #define QNN_CASE32_U(WM_, WN_)                                                                  \
-            if (wm == WM_ && wn == WN_) {                                                       \
-                static bool attr_set = false;                                                   \
-                auto *k = conv_m32_kernel<BITS, WM_, WN_, true, false, 8, false, true>;         \
-                if (!attr_set) {                                                                \
-                    if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize, \
-                                            a.lds_bytes > 64 * 1024 ? 160 * 1024 : 64 * 1024) != hipSuccess) \
-                        (void)hipGetLastError();                                                \
-                    attr_set = true;                                                            \
-                }                                                                               \
-                hipLaunchKernelGGL(k, grid, dim3(512), a.lds_bytes, s, a);                      \
-                return hipGetLastError();                                                       \
-            }
-            QNN_CASE32_U(1, 1) QNN_CASE32_U(2, 1) QNN_CASE32_U(1, 2) QNN_CASE32_U(2, 2)
+        QNN_CASE32_XU(WM_, WN_, 1, false, 4, true) QNN_CASE32_XU(WM_, WN_, 1, true, 4, true)    \
+        QNN_CASE32_XU(WM_, WN_, 1, false, 8, true)
+        QNN_CASE32_U(1, 1) QNN_CASE32_U(2, 1) QNN_CASE32_U(1, 2) QNN_CASE32_U(2, 2)
 #undef QNN_CASE32_U
-        }
     }
     QNN_CASE32(1, 1, 0) QNN_CASE32(1, 2, 0) QNN_CASE32(2, 1, 0) QNN_CASE32(2, 2, 0)
     QNN_CASE32(1, 1, 1) QNN_CASE32(1, 2, 1) QNN_CASE32(2, 1, 1) QNN_CASE32(2, 2, 1)
@@ -884,6 +875,7 @@ hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, int
     }
 #undef QNN_CASE32
 #undef QNN_CASE32_X
+#undef QNN_CASE32_XU
     return hipErrorInvalidValue;
 }
 

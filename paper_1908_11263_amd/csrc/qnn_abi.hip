@@ -308,7 +308,13 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
         return QNN_ERR_UNSUPPORTED;
     b.ksteps = 2 * ((b.kchunks + 3) / 4);  // an even number of 32-deep steps
     b.kch = 2 * b.ksteps;
-    const int cb = f4 ? 16 : 2 * bits;  // LDS bytes of a filter row per 16-byte K chunk
+    // 4-bit filters walked tap by tap are staged unpacked to int8: the main
+    // loop then spends no vector instructions expanding them, for twice the
+    // filter bytes in LDS (measured faster at 4 bits; at 2 bits the fourfold
+    // filter bytes cost more than the expansion)
+    const bool unpack = !f4 && bits == 4 && al16;
+    b.wunpack = unpack ? 1 : 0;
+    const int cb = (f4 || unpack) ? 16 : 2 * bits;  // LDS bytes of a filter row per 16-byte K chunk
     b.kp = (b.kch + 1) * cb;         // odd multiple of cb: conflict-free fragment reads
     const int obits = b.epi == EPI_RAW32 ? 32 : bits;
     const int64_t tab_bytes = 3 * 4 * (int64_t)b.kch;
@@ -368,17 +374,9 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
             if (allow_nw8 && !a.pool && a.epi != EPI_STAIR && wm <= 2 && al16 &&
                 units <= 2 * kPlanCus) {
                 ConvArgs c8 = b;
-                // 4-bit filters staged unpacked (16-byte chunks per row): the
-                // main loop then spends no vector instructions expanding them,
-                // for twice the filter bytes in LDS (measured faster at 4 bits;
-                // at 2 bits the fourfold filter bytes cost more than they save)
-                const bool unpack = !f4 && bits == 4;
-                if (unpack)
-                    c8.kp = (b.kch + 1) * 16;
-                const int64_t lds8 = fit_tile(c8, MT, 256 * cwn, bits, obits, (int64_t)MT * c8.kp, tab_bytes, true);
+                const int64_t lds8 = fit_tile(c8, MT, 256 * cwn, bits, obits, (int64_t)MT * b.kp, tab_bytes, true);
                 if (lds8 >= 0 && lds8 <= kLdsBytes) {
                     a = c8;
-                    a.wunpack = unpack ? 1 : 0;
                     nw = 8;
                 }
             }
