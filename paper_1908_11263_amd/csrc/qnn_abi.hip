@@ -386,6 +386,53 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
     return QNN_ERR_UNSUPPORTED;
 }
 
+// One-word-pixel kernel (conv_px4_kernel): input pixels of exactly 4 packed
+// bytes, stride 1, 3x3 or 5x5 filters, output rows of at most 32 pixels,
+// images of at most 2048 pixels, scale-and-clamp (pooled or not) or raw
+// outputs, channel groups that fill whole output words, and an image tile
+// that fits 64 KB of LDS with the output staging.  Fills everything but the
+// pointers and ypb; false when the layer does not qualify.
+bool plan_px4(Px4Args &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g, const qnn_epi *e,
+              int32_t ho, int32_t wo, bool pool)
+{
+    const int bits = x->bits;
+    if (bits != 8 && bits != 4 && bits != 2)
+        return false;
+    if (pixel_bytes64(x) != 4 || g->stride_h != 1 || g->stride_w != 1)
+        return false;
+    if (!(g->kh == g->kw && (g->kh == 3 || g->kh == 5)))
+        return false;
+    if (wo > 32 || (int64_t)x->h * x->w > 2048)
+        return false;
+    if (!(e->kind == QNN_EPI_REQUANT || (e->kind == QNN_EPI_RAW32 && !pool)))
+        return false;
+    if (((int64_t)m * bits) % 32 != 0)
+        return false;
+    const int ub = 32 / bits;                 // staged bytes per pixel
+    const int pp = 32 + g->kw - 1;            // tile pitch, pixels
+    const int dy = (g->kh + 1) / 2;           // filter rows per half band
+    const int64_t rows = 2 * (int64_t)((ho + 1) / 2) + 2 * dy - 1;
+    const int64_t tile = (rows * pp * ub + 15) & ~(int64_t)15;
+    if (tile + 4 * (pool ? 16 : 32) * 32 > 64 * 1024)
+        return false;
+    memset(&p, 0, sizeof(p));
+    p.bias = e->bias;
+    p.mult = e->mult;
+    p.shift = e->shift;
+    p.n = x->n; p.h = x->h; p.w_ = x->w; p.m = m;
+    p.ph = g->pad_h; p.pw = g->pad_w; p.ho = ho; p.wo = wo;
+    p.epi = e->kind;
+    p.clip_lo = e->clip_lo;
+    p.clip_hi = e->clip_hi;
+    p.pool = pool ? 1 : 0;
+    p.hp = ho / 2;
+    p.wp = wo / 2;
+    p.tile_bytes = (int32_t)tile;
+    p.quads = ((int64_t)x->h * x->w) % 4 == 0 ? 1 : 0;
+    p.div_w = make_fastdiv((uint32_t)x->w);
+    return true;
+}
+
 qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const void *w_dev,
                     const qnn_conv_geom *g, const qnn_epi *e, const qnn_tensor *y, void *y_dev,
                     void *stream, bool pool = false, const qnn_tile *force = nullptr)
@@ -478,6 +525,31 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
         a.div_cd = make_fastdiv((uint32_t)a.cd);
         a.div_kw = make_fastdiv((uint32_t)a.kw);
         return launch_conv_xnor(a, s) == hipSuccess ? QNN_OK : QNN_ERR_LAUNCH;
+    }
+
+    // layers whose input pixel is one packed word (a network's first layer):
+    // the dedicated kernel, unless the caller forces another tile
+    const bool force_px4 = force && force->kernel == QNN_TILE_PX4;
+    if (!f4 && (!force || force_px4)) {
+        Px4Args p;
+        if (plan_px4(p, x, m, g, e, ho, wo, pool)) {
+            st = device_info(&cus);
+            if (st != QNN_OK)
+                return st;
+            p.x = (const uint32_t *)x_dev;
+            p.w = (const uint8_t *)w_dev;
+            p.y = (uint8_t *)y_dev;
+            p.ypb = ypb;
+            // four workgroups per compute unit, each walking whole images
+            int64_t gx = (int64_t)cus * 4;
+            if (gx > x->n)
+                gx = x->n;
+            dim3 grid((unsigned)gx, (unsigned)((m + 31) / 32));
+            return launch_conv_px4(p, x->bits, g->kh, g->kw, grid, s) == hipSuccess ? QNN_OK
+                                                                                  : QNN_ERR_LAUNCH;
+        }
+        if (force_px4)
+            return QNN_ERR_UNSUPPORTED;
     }
 
     ConvArgs a;
@@ -689,6 +761,8 @@ qnn_status qnn_conv2d_tiled(const qnn_tensor *x, const void *x_dev, int32_t m, c
             return QNN_ERR_BITS;
         built = (tm == 0 && tn == 0 && tile->waves == 0) ||
                 ((tile->waves == 4 || tile->waves == 8) && (tn == 1 || tn == 2) && (tm == 1 || tm == 2));
+    } else if (tile->kernel == QNN_TILE_PX4) {
+        built = tm == 0 && tn == 0 && tile->waves == 0;
     } else if (tile->kernel == 16)
         built = tile->waves == 4 && (tm == 1 || tm == 2 || tm == 4) && (tn == 1 || tn == 2 || tn == 4);
     else if (tile->kernel == 32)

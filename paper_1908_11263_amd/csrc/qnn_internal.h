@@ -78,6 +78,24 @@ struct ConvArgs {
     int32_t wunpack;       // 32x32 kernel: 4-/2-bit filters staged unpacked to int8
 };
 
+// Arguments of the one-word-pixel convolution (conv_px4_kernel): input
+// pixels of exactly 4 packed bytes, stride 1, output rows of at most 32
+// pixels; one workgroup walks whole images, one 32-channel group per
+// grid row.
+struct Px4Args {
+    const uint32_t *x;     // packed NHWC input, one word per pixel
+    const uint8_t *w;      // packed OHWI weights, one word per tap
+    uint8_t *y;            // packed NHWC codes (pooled or not) or int32 [pix][M]
+    const int32_t *bias, *mult;
+    const int8_t *shift;
+    int32_t n, h, w_, m, ph, pw, ho, wo;
+    int32_t epi, clip_lo, clip_hi, ypb;
+    int32_t pool, hp, wp;
+    int32_t tile_bytes;    // LDS bytes of the padded, unpacked image tile
+    int32_t quads;         // 1: the image is loaded as 16-byte quads (h*w % 4 == 0)
+    FastDiv div_w;
+};
+
 // Arguments of the INT-1 XNOR/popcount convolution.
 struct XnorArgs {
     const uint32_t *x;     // packed NHWC bits, cd dwords per pixel
@@ -112,6 +130,8 @@ hipError_t launch_conv_m32_b2(const ConvArgs &a, int wm, int wn, int al16, int n
 hipError_t launch_conv_m32_f4(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_m32_f4b1(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s);
+// returns hipErrorInvalidValue for a (bits, kh, kw) with no built instance
+hipError_t launch_conv_px4(const Px4Args &a, int bits, int kh, int kw, dim3 grid, hipStream_t s);
 hipError_t launch_maxpool(const PoolArgs &a, int bits, hipStream_t s);
 hipError_t launch_relu_s8(const uint8_t *x, uint8_t *y, size_t count, hipStream_t s);
 

@@ -25,7 +25,7 @@ def test_exports_every_header_function(q, L):
     assert len(names) >= 12
     for name in names:
         assert hasattr(L, name), name
-    assert L.qnn_abi_version() == 5
+    assert L.qnn_abi_version() == 6
 
 
 def test_status_strings(q, L):
@@ -266,3 +266,29 @@ def test_conv_fp4_validation(q, L):
     # 9 * 310720 = 2796480 > 2^24 / 6: partial sums could leave the exact fp32 range
     big = ((1, 3, 3, 310720), 2, 32, g, REQ2, (1, 3, 3, 32, 2))
     assert call_conv_tiled(q, L, *big, (fp4, 0, 0, 0)) == 6
+
+
+def test_conv_px4_validation(q, L):
+    """The one-word-pixel kernel (QNN_TILE_PX4): only the (0, 0, 0) shape,
+    only for layers it covers (refused on the host otherwise)."""
+    px4 = q.TILE_PX4
+    REQ2 = (0, None, FAKE, FAKE, None, 0, 3)
+    g5 = (5, 5, 1, 1, 2, 2)
+    ok8 = ((2, 32, 32, 4), 8, 32, g5, REQ8, (2, 32, 32, 32, 8))
+    assert call_conv_tiled(q, L, *ok8, (px4, 0, 0, 0)) == 8               # valid: no GPU here
+    assert call_conv_tiled(q, L, (2, 16, 16, 16), 2, 32, (3, 3, 1, 1, 1, 1), REQ2,
+                           (2, 16, 16, 32, 2), (px4, 0, 0, 0)) == 8
+    for tile in [(px4, 1, 0, 0), (px4, 0, 1, 0), (px4, 0, 0, 4)]:
+        assert call_conv_tiled(q, L, *ok8, tile) == 4, tile               # not built
+    refused = [
+        ((1, 9, 9, 4), 8, 32, (3, 3, 2, 2, 1, 1), REQ8, (1, 5, 5, 32, 8)),     # stride 2
+        ((1, 9, 9, 8), 8, 32, (3, 3, 1, 1, 1, 1), REQ8, (1, 9, 9, 32, 8)),     # 8-byte pixels
+        ((1, 9, 40, 4), 8, 32, (3, 3, 1, 1, 1, 1), REQ8, (1, 9, 40, 32, 8)),   # 40 outputs per row
+        ((1, 9, 9, 4), 8, 32, (7, 7, 1, 1, 3, 3), REQ8, (1, 9, 9, 32, 8)),     # 7x7 filter
+        ((1, 9, 9, 16), 2, 24, (3, 3, 1, 1, 1, 1), REQ2, (1, 9, 9, 24, 2)),    # 48-bit output pixels
+        ((1, 65, 32, 4), 8, 32, (3, 3, 1, 1, 1, 1), REQ8, (1, 65, 32, 32, 8)),  # 2080 pixels
+    ]
+    for args in refused:
+        assert call_conv_tiled(q, L, *args, (px4, 0, 0, 0)) == 7, args
+    assert call_conv_tiled(q, L, (1, 8, 8, 32), 1, 32, (3, 3, 1, 1, 1, 1),
+                           (1, None, None, None, FAKE, 0, 0), (1, 8, 8, 32, 1), (px4, 0, 0, 0)) == 4

@@ -1,0 +1,169 @@
+"""GPU parity of the one-word-pixel convolution kernel (QNN_TILE_PX4: layers
+whose input pixel is one packed 32-bit word, e.g. a network's first layer)
+against the CPU oracle, byte for byte: plain and pooled scale-and-clamp,
+raw accumulators, every compression-plan mode (including multipliers that
+are not positive, where pooling must follow the compression), odd and
+ragged image sizes, images loaded word by word, many images per
+workgroup, and layers the kernel must refuse."""
+import numpy as np
+import pytest
+
+import synth
+from gpu_helpers import EPI, dev, log, oracle_conv, threads
+
+pytestmark = pytest.mark.gpu
+
+PX4 = (1, 0, 0, 0)
+
+
+@pytest.fixture(scope="module")
+def qnn():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_1908_11263_amd as q
+    q.device_check()
+    return q
+
+
+def layer(bits, n, h, w, m, k, pad, seed, epi="requant", mult_rng=(1, 1 << 10), shift=10,
+          clip=None):
+    """One-word pixels: 32/bits channels."""
+    hi = (1 << bits) - 1
+    whi = (1 << (bits - 1)) - 1
+    c = 32 // bits
+    return synth.conv_layer("px4_int%d" % bits, bits, n, h, w, c, m, k, pad, seed, (0, hi),
+                            (-(1 << (bits - 1)), whi), bias_rng=(-hi * 50, hi * 50),
+                            mult_rng=mult_rng, shift=shift, clip=clip or (0, hi), epi=epi)
+
+
+def run(qnn, L, pool=False, tile=None, epi=None):
+    import torch
+    epi = epi or L.epi
+    args = (dev(L.x), (L.n, L.h, L.w, L.c), L.bits, dev(L.wt), L.m, L.kh, L.kw, L.stride, L.pad, epi)
+    kw = dict(bias=dev(L.bias), mult=dev(L.mult), shift=dev(L.shift), clip=L.clip)
+    if pool:
+        assert tile is None
+        y = qnn.conv2d_maxpool(*args, **kw)
+    else:
+        y = qnn.conv2d(*args, tile=tile, **kw)
+    torch.cuda.synchronize()
+    return y.cpu().numpy()
+
+
+def want(orc, L, pool=False, epi=None):
+    y = oracle_conv(orc, L, epi=epi)
+    if pool:
+        y = orc.maxpool2d(y, (L.n, L.ho, L.wo, L.m), L.bits, 2, 2, 2, 2)
+    return y
+
+
+def check(qnn, orc, L, pool=False, epi=None, tile=None):
+    log("case", L.name, epi or L.epi, "pool" if pool else "", "tile", tile,
+        "N=%d H=%d W=%d M=%d k=%d p=%s" % (L.n, L.h, L.w, L.m, L.kh, L.pad))
+    got = run(qnn, L, pool=pool, tile=tile, epi=epi)
+    ref = want(orc, L, pool=pool, epi=epi)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    bad = np.argwhere(got != ref)
+    assert bad.size == 0, "%s: %d mismatches, first at %s" % (L.name, len(bad), bad[:5].tolist())
+
+
+# (n, h, w, m, k, pad): CIFAR-like first layers, narrow outputs, odd and
+# ragged sizes (h*w not a multiple of 4: word-by-word image loads), wide
+# padding, several channel groups
+SHAPES = [
+    (3, 32, 32, 32, 5, 2),
+    (5, 28, 28, 64, 5, 0),
+    (2, 17, 13, 96, 3, 1),
+    (7, 8, 8, 32, 3, 3),
+    (1, 30, 32, 48, 5, 2),
+    (4, 9, 31, 16, 3, 0),
+    (2, 1, 1, 32, 3, 1),
+]
+
+
+@pytest.mark.parametrize("bits", [8, 4, 2])
+@pytest.mark.parametrize("pool", [False, True])
+def test_px4_requant(qnn, orc, bits, pool):
+    for i, (n, h, w, m, k, pad) in enumerate(SHAPES):
+        if m * bits % 32:
+            continue
+        L = layer(bits, n, h, w, m, k, pad, seed=100 * bits + i)
+        if pool and (L.ho < 2 or L.wo < 2):
+            continue
+        check(qnn, orc, L, pool=pool)
+        if not pool:
+            # the library's choice is this kernel: forcing it gives the same bytes
+            check(qnn, orc, L, tile=PX4)
+
+
+@pytest.mark.parametrize("bits", [8, 4, 2])
+def test_px4_raw32(qnn, orc, bits):
+    for i, (n, h, w, m, k, pad) in enumerate(SHAPES):
+        if m * bits % 32:
+            continue
+        check(qnn, orc, layer(bits, n, h, w, m, k, pad, seed=7 + i), epi="raw32")
+
+
+@pytest.mark.parametrize("bits", [8, 4, 2])
+def test_px4_plan_modes(qnn, orc, bits):
+    """Multipliers above 2^shift (the general plan forms), shift 0 and clip
+    bounds inside the code range, and multipliers that are zero or negative
+    (the compression is not monotone: codes are pooled after it)."""
+    hi = (1 << bits) - 1
+    cases = [dict(mult_rng=(1 << 12, 1 << 14), shift=8),
+             dict(mult_rng=(1, 3), shift=0, clip=(1, hi - 1) if hi > 2 else (0, hi)),
+             dict(mult_rng=(-(1 << 10), 1 << 10), shift=9),
+             dict(mult_rng=((1 << 30), (1 << 31) - 1), shift=40)]
+    for j, kw in enumerate(cases):
+        L = layer(bits, 3, 12, 14, 32, 3, 1, seed=50 + j, **kw)
+        check(qnn, orc, L)
+        check(qnn, orc, L, pool=True)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_px4_many_images(qnn, orc, bits):
+    """More images than workgroups: every workgroup walks several images
+    with the next image's words prefetched."""
+    L = layer(bits, 2500, 16, 16, 32, 3, 1, seed=bits)
+    check(qnn, orc, L, pool=True)
+
+
+def test_px4_equals_general_kernels(qnn, orc):
+    """The same layer through the one-word-pixel kernel and through the
+    general 32x32 and 16x16 tiles."""
+    for bits in (8, 4, 2):
+        L = layer(bits, 2, 32, 32, 32, 5, 2, seed=bits)
+        ref = want(orc, L)
+        for tile in (PX4, (32, 1, 2, 4), (16, 2, 1, 4)):
+            assert np.array_equal(run(qnn, L, tile=tile), ref), (bits, tile)
+
+
+def test_px4_refuses_layers_it_does_not_cover(qnn, orc):
+    """Forced on a layer outside its domain the kernel is refused with
+    QNN_ERR_UNSUPPORTED (7); the library's own choice still matches."""
+    L8 = layer(8, 1, 9, 9, 32, 3, 1, seed=1)
+    outside = [
+        synth.conv_layer("px4_stride2", 8, 1, 9, 9, 4, 32, 3, 1, 2, (0, 255), (-128, 127),
+                         bias_rng=(-99, 99), mult_rng=(1, 1 << 10), shift=10, clip=(0, 255),
+                         stride=2),                                        # stride 2
+        synth.conv_layer("px4_c8", 8, 1, 9, 9, 8, 32, 3, 1, 2, (0, 255), (-128, 127),
+                         bias_rng=(-99, 99), mult_rng=(1, 1 << 10), shift=10, clip=(0, 255)),  # 8-byte pixels
+        layer(8, 1, 9, 40, 32, 3, 1, seed=2),                              # rows of 40 outputs
+        layer(8, 1, 9, 9, 32, 1, 0, seed=3),                               # 1x1 filter
+        layer(2, 1, 9, 9, 24, 3, 1, seed=4),                               # 24 channels at 2 bits
+    ]
+    for L in outside:
+        with pytest.raises(qnn.QnnError) as e:
+            run(qnn, L, tile=PX4)
+        assert e.value.status == 7, L.name
+        check(qnn, orc, L)
+    with pytest.raises(qnn.QnnError) as e:
+        run(qnn, with_stair(L8), tile=PX4)
+    assert e.value.status in (2, 7)
+
+
+def with_stair(L):
+    return synth.ConvLayer(L.name + "_stair", L.bits, L.n, L.h, L.w, L.c, L.m, L.kh, L.kw,
+                           L.stride, L.pad, "stair", L.x_vals, L.w_vals, L.bias, None, None,
+                           np.zeros((L.m, (1 << L.bits) - 1), np.int32), L.clip, L.c_alg)
