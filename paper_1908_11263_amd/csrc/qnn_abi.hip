@@ -390,7 +390,7 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
 // bytes, stride 1, 3x3 or 5x5 filters, output rows of at most 32 pixels,
 // images of at most 2048 pixels, scale-and-clamp (pooled or not) or raw
 // outputs, channel groups that fill whole output words, and an image tile
-// that fits 64 KB of LDS with the output staging.  Fills everything but the
+// that fits 64 KB of LDS.  Fills everything but the
 // pointers and ypb; false when the layer does not qualify.
 bool plan_px4(Px4Args &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g, const qnn_epi *e,
               int32_t ho, int32_t wo, bool pool)
@@ -408,12 +408,12 @@ bool plan_px4(Px4Args &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g
         return false;
     if (((int64_t)m * bits) % 32 != 0)
         return false;
-    const int ub = 32 / bits;                 // staged bytes per pixel
-    const int pp = 32 + g->kw - 1;            // tile pitch, pixels
+    const int sb = bits == 8 ? 8 : 32 / bits; // tile slot bytes (8 bits: a pixel pair)
+    const int pp = 32 + g->kw - 1;            // tile pitch, slots
     const int dy = (g->kh + 1) / 2;           // filter rows per half band
     const int64_t rows = 2 * (int64_t)((ho + 1) / 2) + 2 * dy - 1;
-    const int64_t tile = (rows * pp * ub + 15) & ~(int64_t)15;
-    if (tile + 4 * (pool ? 16 : 32) * 32 > 64 * 1024)
+    const int64_t tile = (rows * pp * sb + 15) & ~(int64_t)15;
+    if (tile > 64 * 1024)
         return false;
     memset(&p, 0, sizeof(p));
     p.bias = e->bias;
@@ -540,13 +540,8 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
             p.w = (const uint8_t *)w_dev;
             p.y = (uint8_t *)y_dev;
             p.ypb = ypb;
-            // four workgroups per compute unit, each walking whole images
-            int64_t gx = (int64_t)cus * 4;
-            if (gx > x->n)
-                gx = x->n;
-            dim3 grid((unsigned)gx, (unsigned)((m + 31) / 32));
-            return launch_conv_px4(p, x->bits, g->kh, g->kw, grid, s) == hipSuccess ? QNN_OK
-                                                                                  : QNN_ERR_LAUNCH;
+            return launch_conv_px4(p, x->bits, g->kh, g->kw, cus, s) == hipSuccess ? QNN_OK
+                                                                                 : QNN_ERR_LAUNCH;
         }
         if (force_px4)
             return QNN_ERR_UNSUPPORTED;

@@ -130,8 +130,9 @@ hipError_t launch_conv_m32_b2(const ConvArgs &a, int wm, int wn, int al16, int n
 hipError_t launch_conv_m32_f4(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_m32_f4b1(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s);
-// returns hipErrorInvalidValue for a (bits, kh, kw) with no built instance
-hipError_t launch_conv_px4(const Px4Args &a, int bits, int kh, int kw, dim3 grid, hipStream_t s);
+// returns hipErrorInvalidValue for a (bits, kh, kw) with no built instance;
+// the grid fills the cus compute units with resident workgroups
+hipError_t launch_conv_px4(const Px4Args &a, int bits, int kh, int kw, int cus, hipStream_t s);
 hipError_t launch_maxpool(const PoolArgs &a, int bits, hipStream_t s);
 hipError_t launch_relu_s8(const uint8_t *x, uint8_t *y, size_t count, hipStream_t s);
 
