@@ -96,16 +96,17 @@ __global__ void __launch_bounds__(256) conv_xnor_kernel(const uint32_t *__restri
     }
 }
 
-// Register-resident variant (kd a multiple of 8): a lane gathers its whole
-// im2col column (kd <= KDM words, zero bits for padding taps) once, then
-// walks the output channels of its workgroup's channel group (the split
-// over workgroups keeps several waves per SIMD to hide the scalar-load
-// latency).  Channel m's kd filter words arrive by scalar loads one 8-word
-// block ahead of their use.  The lane counts mismatching bits,
+// Register-resident variant (filter volume KD words, a multiple of 8, known
+// at compile time): a lane gathers its whole im2col column (zero bits for
+// padding taps) once, then walks the output channels of its workgroup's
+// channel group (the split over workgroups keeps several waves per SIMD to
+// hide the scalar-load latency).  Channel m's KD filter words arrive by
+// scalar loads in 8-word blocks that alternate between two register sets,
+// one block ahead of their use.  The lane counts mismatching bits,
 // popcount(x ^ w): with K taps of +-1 values, the dot product is
 // K - 2 * mismatches, so no complement is needed (two vector instructions
-// per 32 binary MACs).
-template <int KDM>
+// per 32 binary MACs, and with KD fixed no scalar bookkeeping per block).
+template <int KD>
 __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__restrict__ xg,
                                                             const uint32_t *__restrict__ wgl,
                                                             const int32_t *__restrict__ bias,
@@ -124,16 +125,41 @@ __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__re
     const int n = (int)fdiv((uint32_t)q, a.div_ho);
     const int oy = q - n * a.ho;
 
-    uint32_t xv[KDM];
+    // the lane's im2col column: taps in (ky, kx) order, cd words each
+    uint32_t xv[KD];
+    if ((a.cd & 3) == 0) {
+        // whole 16-byte quads: the tap position advances in wave-uniform steps
+        int tap = 0, d = 0, ky = 0, kx = 0;
 #pragma unroll
-    for (int k = 0; k < KDM; ++k) {
-        xv[k] = 0u;
-        if (k < a.kd) {
+        for (int k = 0; k < KD; k += 4) {
+            const int iy = oy * a.sh - a.ph + ky, ix = ox * a.sw - a.pw + kx;
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if ((uint32_t)iy < (uint32_t)a.h && (uint32_t)ix < (uint32_t)a.w_)
+                v = *(const uint4 *)(xg + ((size_t)(n * a.h + iy) * a.w_ + ix) * a.cd + d);
+            xv[k] = v.x;
+            xv[k + 1] = v.y;
+            xv[k + 2] = v.z;
+            xv[k + 3] = v.w;
+            d += 4;
+            if (d == a.cd) {
+                d = 0;
+                ++tap;
+                if (++kx == a.kw) {
+                    kx = 0;
+                    ++ky;
+                }
+            }
+        }
+        (void)tap;
+    } else {
+#pragma unroll
+        for (int k = 0; k < KD; ++k) {
             const int tap = (int)fdiv((uint32_t)k, a.div_cd);
             const int d = k - tap * a.cd;
             const int ky = (int)fdiv((uint32_t)tap, a.div_kw);
             const int kx = tap - ky * a.kw;
             const int iy = oy * a.sh - a.ph + ky, ix = ox * a.sw - a.pw + kx;
+            xv[k] = 0u;
             if (iy >= 0 && iy < a.h && ix >= 0 && ix < a.w_)
                 xv[k] = xg[((n * a.h + iy) * a.w_ + ix) * a.cd + d];
         }
@@ -149,39 +175,36 @@ __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__re
         const int mn = m + 1 < me ? m + 1 : m;
         const int32_t b_next = bias ? bias[mn] : 0;
         const int32_t t_next = a.epi == EPI_RAW32 ? 0 : thresh[mn];
-        // kd is a multiple of 8: the filter row is walked in 32-byte blocks.
         // Block b + 1 is requested after the first word of block b is used:
         // a wait for scalar loads covers every load in flight, so requesting
         // it earlier would make the wait for block b also wait for b + 1.
-        // The scheduling barriers keep this order (and keep the compiler from
-        // hoisting every block's scalar loads, which would spill scalar
-        // registers).  Each word costs one xor and one accumulating popcount;
-        // the empty asm keeps the additions from being regrouped into
-        // three-input adds, which would cost one more instruction per two
-        // words.
-        const uint4 *wr = (const uint4 *)(wgl + (size_t)m * a.kd);
-        uint4 c0 = wr[0], c1 = wr[1];
+        // The scheduling barriers keep this order; the empty asm keeps the
+        // accumulating popcounts from being regrouped into three-input adds.
+        const uint4 *wr = (const uint4 *)(wgl + (size_t)m * KD);
+        uint4 s0 = wr[0], s1 = wr[1], t0, t1;
         uint32_t mis = 0;
 #pragma unroll
-        for (int kb = 0; kb < KDM; kb += 8) {
-            if (kb < a.kd) {
-                const uint32_t w8[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
-                mis = __popc(xv[kb] ^ w8[0]) + mis;
-                __asm__("" : "+v"(mis));
-                __builtin_amdgcn_sched_barrier(0);
-                uint4 n0 = c0, n1 = c1;
-                if (kb + 8 < a.kd) {
-                    n0 = wr[(kb + 8) / 4];
-                    n1 = wr[(kb + 8) / 4 + 1];
+        for (int kb = 0; kb < KD; kb += 8) {
+            const bool odd = (kb >> 3) & 1;
+            const uint4 c0 = odd ? t0 : s0, c1 = odd ? t1 : s1;
+            const uint32_t w8[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+            mis = __popc(xv[kb] ^ w8[0]) + mis;
+            __asm__("" : "+v"(mis));
+            __builtin_amdgcn_sched_barrier(0);
+            if (kb + 8 < KD) {
+                if (odd) {
+                    s0 = wr[(kb + 8) / 4];
+                    s1 = wr[(kb + 8) / 4 + 1];
+                } else {
+                    t0 = wr[(kb + 8) / 4];
+                    t1 = wr[(kb + 8) / 4 + 1];
                 }
-                __builtin_amdgcn_sched_barrier(0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int i = 1; i < 8; ++i) {
-                    mis = __popc(xv[kb + i] ^ w8[i]) + mis;
-                    __asm__("" : "+v"(mis));
-                }
-                c0 = n0;
-                c1 = n1;
+            for (int i = 1; i < 8; ++i) {
+                mis = __popc(xv[kb + i] ^ w8[i]) + mis;
+                __asm__("" : "+v"(mis));
             }
             __builtin_amdgcn_sched_barrier(0);
         }
@@ -215,18 +238,18 @@ hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s)
     dim3 grid((a.npix + 255) / 256);
     // channel groups of mgrp (a multiple of 32) along grid.y
     dim3 grid_res(grid.x * a.ngroups);
-    if (a.kd % 8 != 0 || a.kd > 128)
-        ;
-    else if (a.kd <= 32)
-        hipLaunchKernelGGL(conv_xnor_res_kernel<32>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
-    else if (a.kd <= 64)
-        hipLaunchKernelGGL(conv_xnor_res_kernel<64>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
-    else if (a.kd <= 72)  // 3x3 taps of 256 channels
-        hipLaunchKernelGGL(conv_xnor_res_kernel<72>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
-    else if (a.kd <= 96)
-        hipLaunchKernelGGL(conv_xnor_res_kernel<96>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
-    else
-        hipLaunchKernelGGL(conv_xnor_res_kernel<128>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias, a.thresh, a);
+    if (a.kd % 8 == 0 && a.kd <= 128) {
+        switch (a.kd / 8) {
+#define QNN_XR(J_)                                                                                          \
+        case J_:                                                                                            \
+            hipLaunchKernelGGL(conv_xnor_res_kernel<8 * J_>, grid_res, dim3(256), 0, s, a.x, a.w, a.bias,  \
+                               a.thresh, a);                                                                \
+            break;
+            QNN_XR(1) QNN_XR(2) QNN_XR(3) QNN_XR(4) QNN_XR(5) QNN_XR(6) QNN_XR(7) QNN_XR(8)
+            QNN_XR(9) QNN_XR(10) QNN_XR(11) QNN_XR(12) QNN_XR(13) QNN_XR(14) QNN_XR(15) QNN_XR(16)
+#undef QNN_XR
+        }
+    }
     if (a.kd % 8 == 0 && a.kd <= 128)
         return hipGetLastError();
     if (a.cd % 8 == 0)
