@@ -255,3 +255,16 @@ def test_int1_register_resident_shapes(qnn, orc):
     for (c, k, m) in [(256, 1, 40), (64, 2, 32), (256, 3, 64), (128, 4, 33), (512, 2, 70),
                       (1024, 1, 8), (256, 4, 32), (128, 5, 32)]:
         check_layer(orc, make(1, 2, 7, 6, c, m, k, pad=k // 2))
+
+
+def test_int1_every_register_resident_volume(qnn, orc):
+    """Every filter volume the register-resident XNOR kernel is built for
+    (8..128 words in steps of 8), through the quad-wide im2col gather
+    (channel words a multiple of 4) and the word-by-word one, with binary
+    threshold and raw outputs."""
+    cases = [(256 * j, 1) for j in range(1, 17)]            # 1x1 filters, 8j words per pixel
+    cases += [(64, 2), (192, 2), (64, 4), (320, 2), (64, 6), (96, 4)]  # 2 or 6 words per tap
+    for i, (c, k) in enumerate(cases):
+        L = make(1, 1, 5, 6, c, 40, k, pad=k // 2, seed=100 + i)
+        check_layer(orc, L)
+        check_layer(orc, L, epi="raw32")
