@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define QNN_ABI_VERSION 6
+#define QNN_ABI_VERSION 7
 
 typedef enum {
     QNN_OK = 0,
@@ -124,15 +124,17 @@ typedef struct {
  * QNN_EPI_THRESH1 or QNN_EPI_RAW32 as on the XNOR path.  The library never
  * picks this path by itself. */
 #define QNN_TILE_FP4 4
-/* Layers whose input pixel is one packed 32-bit word (a network's first
- * layer: e.g. 3 image channels padded to 4 at 8 bits), stride 1, 3x3 or 5x5
- * filters, output rows of at most 32 pixels, images of at most 2048 pixels,
- * QNN_EPI_REQUANT (also fused with max-pooling) or QNN_EPI_RAW32, M*bits a
- * multiple of 32: a kernel that keeps the filters in registers and the whole
- * padded image in local memory.  The library picks it by itself for every
- * layer that qualifies; tile_m = tile_n = waves = 0.  A layer that does not
- * qualify gives QNN_ERR_UNSUPPORTED. */
-#define QNN_TILE_PX4 1
+/* Small images, a workgroup keeping whole padded images in local memory and
+ * its filters in registers: stride 1, 3x3 or 5x5 filters, output rows of at
+ * most 32 pixels, images of at most 8 KB, QNN_EPI_REQUANT (also fused with
+ * max-pooling) or QNN_EPI_RAW32, M*bits a multiple of 32, and input pixels
+ * of 4 packed bytes (a network's first layer: e.g. 3 image channels padded
+ * to 4 at 8 bits) or of 16 / 32 packed bytes (32 channels at 4 / 8 bits, 64
+ * at 2 / 4 bits) with at most 28 K steps of 32 (5x5 filters: 32 channels at
+ * 8 or 4 bits).  The library picks it by itself for every layer that
+ * qualifies; tile_m = tile_n = waves = 0.  A layer that does not qualify
+ * gives QNN_ERR_UNSUPPORTED. */
+#define QNN_TILE_IMAGE 1
 
 /* Tile shape of the matrix-core convolution kernels, for exploration and
  * tuning (the library otherwise picks it per layer). */

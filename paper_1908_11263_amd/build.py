@@ -24,10 +24,11 @@ FLAGS = [
 ]
 
 
-# per-source extra flags: the one-word-pixel kernel keeps its MFMA
-# accumulators in ordinary VGPRs (its epilogue reads them right away, and
+# per-source extra flags: the whole-image kernels keep their MFMA
+# accumulators in ordinary VGPRs (their epilogues read them right away, and
 # the accumulation registers would cost copies and occupancy)
-EXTRA = {"conv_px4.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+_VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
+EXTRA = {"conv_img_p4.hip": _VGPR_FORM, "conv_img_p16.hip": _VGPR_FORM, "conv_img_p32.hip": _VGPR_FORM}
 
 
 def sources():

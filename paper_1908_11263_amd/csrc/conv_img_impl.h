@@ -1,0 +1,690 @@
+// Implicit-GEMM quantized convolution for small images: a workgroup keeps
+// whole padded images in LDS and its filters in registers.  Same computation
+// as the other convolution kernels (Sec. III-A Eq. (2), Sec. III-B Eq. (6),
+// scale-and-clamp compression, Sec. IV-A fused max-pooling), laid out for
+// layers whose per-tile bookkeeping would dominate the general kernels: a
+// network's first layer (K = kh*kw*3 for 3 image channels) and the later
+// layers of a small network (16x16 and 8x8 images of 32 channels).
+//   * A workgroup owns one 32-channel group (grid.y) and walks groups of
+//     whole images (several small images per step so that every wave has
+//     work): each padded image is staged once in LDS, unpacked to int8 (8-bit
+//     codes offset by -128, pads included); the next group's bytes are
+//     loaded into registers while the current one is computed.
+//   * The filters of the group live in registers for the whole kernel (one
+//     16-byte fragment per lane and K step), never in LDS.
+//   * A wave computes two MFMA row tiles of 32 output pixels at a time with
+//     v_mfma_i32_32x32x32_i8 (rows = pixels, columns = channels).  A row tile
+//     is 1, 2 or 4 output rows of an image WOP = 32, 16 or 8 pixels wide
+//     (narrower images leave lanes idle), so the lane's pixel is fixed per
+//     tile and every im2col tap is an LDS read at a compile-time offset from
+//     one per-lane base.
+//   * K order.  Pixels of 32 unpacked bytes or more: K steps walk the taps
+//     and the 32-byte chunks of each tap; the two halves of a wave (lanes
+//     0-31, 32-63) take the two 16-byte halves of a chunk.  One-word pixels
+//     (4-16 unpacked bytes): the halves take the filter's upper and lower
+//     band of ceil(kh/2) rows in the same slot order (bands past the filter's
+//     last row and slots past the band carry zero weights); 8-bit tiles then
+//     store a pixel pair per slot, so a run of four taps along a filter row
+//     is two aligned 8-byte reads.
+//   * The 2x2 max-pooling is taken on the accumulators (the compression is
+//     non-decreasing in the accumulator whenever the multiplier is positive,
+//     so the maximum commutes with it) and only the pooled values are
+//     compressed; with a non-positive multiplier each code is compressed
+//     first and the codes are pooled.  The four outputs of a window always
+//     sit in one lane.
+//   * Codes leave as bytes straight from the lanes (4-/2-bit codes of
+//     neighbouring channels packed across lanes with DPP moves), with no
+//     staging through LDS.
+#pragma once
+
+#include "conv_m32_impl.h"
+
+namespace qnn {
+
+// Slot order of the K dimension within one half band (DY filter rows x KW
+// columns) for one-word pixels, TPF taps per 16-byte fragment (U = unpacked
+// bytes per pixel: 4, 8 or 16).  U = 8, 16: the taps in raster order.
+// U = 4 (8-bit codes): first every run of four horizontally adjacent taps of
+// a filter row (one fragment each, read as two aligned 8-byte pixel pairs),
+// then the leftover columns of all rows, four to a fragment.  tap(i) =
+// ky * 256 + kx, or -1 for an empty slot (zero weight, nothing read).
+template <int U, int KW, int DY>
+struct BandTaps {
+    static constexpr int TPF = 16 / U;
+    static constexpr int NT = DY * KW;
+    static constexpr int RUNS = U == 4 ? KW / 4 : 0;
+    static constexpr int LEFT = KW % 4;
+    static constexpr int NR = DY * RUNS;
+    static constexpr int NF = U == 4 ? NR + (DY * LEFT + 3) / 4 : (NT + TPF - 1) / TPF;
+    static constexpr int tap(int i)
+    {
+        if (U != 4)
+            return i < NT ? (i / KW) * 256 + i % KW : -1;
+        const int f = i / 4, t = i % 4;
+        if (f < NR)
+            return (f / (RUNS > 0 ? RUNS : 1)) * 256 + (f % (RUNS > 0 ? RUNS : 1)) * 4 + t;
+        const int j = (f - NR) * 4 + t;
+        return (LEFT > 0 && j < DY * LEFT) ? (j / (LEFT > 0 ? LEFT : 1)) * 256 + RUNS * 4 + j % (LEFT > 0 ? LEFT : 1)
+                                          : -1;
+    }
+};
+
+// Geometry of one instance: BITS-bit codes, pixels of P packed bytes.
+template <int BITS, int P, int KH, int KW, int WOP>
+struct ImgGeom {
+    static constexpr int U = P * 8 / BITS;             // unpacked bytes per pixel
+    static constexpr bool CHUNK = U >= 32;             // K split by 16-byte halves of 32-byte chunks
+    static constexpr int SB = U == 4 ? 8 : U;          // tile slot bytes (8-bit one-word pixels: a pair)
+    static constexpr int PP = WOP + KW - 1;            // tile pitch, slots
+    static constexpr int RB = PP * SB;                 // tile row, bytes
+    static constexpr int RT = 32 / WOP;                // image rows per MFMA row tile
+    static constexpr int DY = (KH + 1) / 2;            // band rows (one-word pixels)
+    static constexpr int CPT = CHUNK ? U / 32 : 1;     // 32-byte chunks per tap
+    typedef BandTaps<CHUNK ? 16 : U, KW, DY> BT;
+    static constexpr int TPF = CHUNK ? 1 : BT::TPF;    // taps per fragment
+    static constexpr int KS = CHUNK ? KH * KW * CPT : BT::NF;  // 32-deep K steps
+    static constexpr int WB = CHUNK ? 16 * BITS / 8 : 4;  // packed filter bytes behind one fragment slot
+};
+
+// One 16-byte im2col fragment for K step S of the pixel whose tile slot is
+// at p (lane half already folded into p): compile-time offsets.
+template <int BITS, int P, int KH, int KW, int WOP, int S>
+__device__ __forceinline__ v4i img_frag(const uint8_t *p)
+{
+    typedef ImgGeom<BITS, P, KH, KW, WOP> G;
+    constexpr int SB = G::SB, PP = G::PP;
+    if constexpr (G::CHUNK) {
+        constexpr int t = S / G::CPT, j = S % G::CPT;
+        return *(const v4i *)(p + ((t / KW) * PP + t % KW) * SB + 32 * j);
+    } else if constexpr (G::U == 4) {
+        typedef typename G::BT TP;
+        uint32_t d[4];
+#pragma unroll
+        for (int t = 0; t < 4; t += 2) {
+            const int t0 = TP::tap(S * 4 + t), t1 = TP::tap(S * 4 + t + 1);
+            if (t0 >= 0 && t1 == t0 + 1) {
+                const uint2 v = *(const uint2 *)(p + ((t0 >> 8) * PP + (t0 & 255)) * SB);
+                d[t] = v.x;
+                d[t + 1] = v.y;
+            } else {
+                d[t] = t0 >= 0 ? *(const uint32_t *)(p + ((t0 >> 8) * PP + (t0 & 255)) * SB) : 0u;
+                d[t + 1] = t1 >= 0 ? *(const uint32_t *)(p + ((t1 >> 8) * PP + (t1 & 255)) * SB) : 0u;
+            }
+        }
+        return (v4i){(int32_t)d[0], (int32_t)d[1], (int32_t)d[2], (int32_t)d[3]};
+    } else if constexpr (G::U == 8) {
+        typedef typename G::BT TP;
+        uint2 d[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            const int tp = TP::tap(S * 2 + t);
+            d[t] = tp >= 0 ? *(const uint2 *)(p + ((tp >> 8) * PP + (tp & 255)) * SB) : make_uint2(0, 0);
+        }
+        return (v4i){(int32_t)d[0].x, (int32_t)d[0].y, (int32_t)d[1].x, (int32_t)d[1].y};
+    } else {
+        typedef typename G::BT TP;
+        constexpr int tp = TP::tap(S);
+        if constexpr (tp >= 0)
+            return *(const v4i *)(p + ((tp >> 8) * PP + (tp & 255)) * SB);
+        else
+            return (v4i){0, 0, 0, 0};
+    }
+}
+
+// Both row tiles' fragments and MFMAs of K steps S .. KS-1 (unrolled through
+// the template recursion, so every offset is an immediate).
+template <int BITS, int P, int KH, int KW, int WOP, int S>
+__device__ __forceinline__ void img_steps(const uint8_t *p0, const uint8_t *p1, const v4i *A, v16i &acc0,
+                                          v16i &acc1)
+{
+    if constexpr (S < ImgGeom<BITS, P, KH, KW, WOP>::KS) {
+        const v4i b0 = img_frag<BITS, P, KH, KW, WOP, S>(p0);
+        const v4i b1 = img_frag<BITS, P, KH, KW, WOP, S>(p1);
+        if constexpr (S == 0) {
+            acc0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b0, A[S], (v16i){}, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b1, A[S], (v16i){}, 0, 0, 0);
+        } else {
+            acc0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b0, A[S], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b1, A[S], acc1, 0, 0, 0);
+        }
+        img_steps<BITS, P, KH, KW, WOP, S + 1>(p0, p1, A, acc0, acc1);
+    }
+}
+
+// Scale-and-clamp code of one (scaled) accumulator from the channel's plan
+// (requant_plan): any mode.
+template <int SL>
+__device__ __forceinline__ uint32_t img_code(int32_t accd, const int4 &e0, const int4 &e1, int32_t lo, int32_t hi)
+{
+    if (e1.z >= 3) {
+        const int32_t d = __builtin_elementwise_sub_sat(accd, e0.x);
+        const uint32_t dc = (uint32_t)min(max(d, 0), e0.y);
+        const uint64_t rs = ((uint64_t)(uint32_t)e1.y << 32) | (uint32_t)e0.w;
+        return (uint32_t)(((uint64_t)dc * (uint32_t)e0.z + rs) >> e1.x);
+    }
+    const int32_t acc32 = accd >> SL;
+    int64_t r;
+    if (e1.z) {
+        const int32_t d = __builtin_elementwise_sub_sat(acc32, e0.x);
+        const uint32_t dc = (uint32_t)min(max(d, 0), e0.y);
+        uint32_t q;
+        if (e1.z == 1)
+            q = (__umul24(dc, (uint32_t)e0.z) + (uint32_t)e0.w) >> e1.y;
+        else
+            q = (uint32_t)(((uint64_t)dc * (uint32_t)e0.z + (uint32_t)e0.w) >> e1.y);
+        r = (int64_t)e1.x + (int64_t)q;
+    } else {
+        const int64_t vv = (int64_t)acc32 + (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);
+        r = round_shift(vv * (int64_t)e0.z, e0.w);
+    }
+    r = r < lo ? lo : (r > hi ? hi : r);
+    return (uint32_t)r;
+}
+
+// Mode-3 plans only (every channel's code fits the 32-bit form): a
+// saturating subtract, a median-of-three clamp to [0, e0.y] (e0.y >= 0), a
+// 24-bit multiply-add and a shift.
+__device__ __forceinline__ uint32_t img_code3(int32_t accd, const int4 &e0, const int4 &e1)
+{
+    const int32_t d = __builtin_elementwise_sub_sat(accd, e0.x);
+    int32_t dc;
+    __asm__("v_med3_i32 %0, %1, 0, %2" : "=v"(dc) : "v"(d), "v"(e0.y));
+    return (__umul24((uint32_t)dc, (uint32_t)e0.z) + (uint32_t)e0.w) >> e1.x;
+}
+
+// Mode-3 and mode-4 plans (the strict form; products up to 64 bits): a
+// saturating subtract, the clamp, one 32x32->64 multiply-add and a shift.
+__device__ __forceinline__ uint32_t img_code4(int32_t accd, const int4 &e0, const int4 &e1)
+{
+    const int32_t d = __builtin_elementwise_sub_sat(accd, e0.x);
+    int32_t dc;
+    __asm__("v_med3_i32 %0, %1, 0, %2" : "=v"(dc) : "v"(d), "v"(e0.y));
+    const uint64_t rs = ((uint64_t)(uint32_t)e1.y << 32) | (uint32_t)e0.w;
+    return (uint32_t)(((uint64_t)(uint32_t)dc * (uint32_t)e0.z + rs) >> e1.x);
+}
+
+// Packs the codes of neighbouring channels into one output byte across
+// lanes (lane = channel): 4 bits, lanes 2k and 2k+1; 2 bits, lanes 4k..4k+3,
+// the lower channel in the lower bits.  Every lane of the wave takes part;
+// the byte is complete on the lanes whose channel is a multiple of 8/BITS.
+template <int BITS>
+__device__ __forceinline__ uint32_t img_pack_lanes(uint32_t code)
+{
+    if (BITS == 8)
+        return code;
+    // quad_perm [1,0,3,2]: the neighbour's code
+    uint32_t v = code | ((uint32_t)__builtin_amdgcn_update_dpp(0, (int)code, 0xB1, 0xF, 0xF, false) << BITS);
+    if (BITS == 2)  // quad_perm [2,3,0,1]: the other pair
+        v |= (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false) << 4;
+    return v;
+}
+
+// 2x2 pooling windows of a pair of row tiles: window k (0..7) holds the
+// registers (tile, v) of its four outputs and its pooled row (relative to
+// the pair's first pooled row) and pooled column (without the lane half's
+// share 2*h, which every window adds).  WOP = 32: a tile is one row, the
+// window spans both tiles; WOP = 16: a tile is two rows, v and v + 8 are one
+// column of both; WOP = 8: a tile is four rows, v and v + 4.
+template <int WOP>
+struct PoolWin {
+    static constexpr int v0(int k)  // first register of window k
+    {
+        return WOP == 32 ? 2 * k : (WOP == 16 ? 2 * (k & 3) : ((k & 2) << 2) + 2 * (k & 1));
+    }
+    static constexpr int t0(int k) { return WOP == 32 ? 0 : k >> 2; }   // tile of the first row
+    static constexpr int t1(int k) { return WOP == 32 ? 1 : k >> 2; }   // tile of the second row
+    static constexpr int dv(int)  // register step from the first row to the second
+    {
+        return WOP == 32 ? 0 : (WOP == 16 ? 8 : 4);
+    }
+    static constexpr int prow(int k) { return WOP == 32 ? 0 : (WOP == 16 ? k >> 2 : 2 * (k >> 2) + ((k >> 1) & 1)); }
+    static constexpr int pcol(int k)
+    {
+        // column of the window's first output (without 4h), halved
+        return WOP == 32 ? 4 * (k >> 1) + (k & 1) : (WOP == 16 ? 4 * ((k & 3) >> 1) + (k & 1) : (k & 1));
+    }
+};
+
+template <int BITS, int P, int KH, int KW, int WOP, bool POOL>
+__global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
+{
+    typedef ImgGeom<BITS, P, KH, KW, WOP> G;
+    constexpr int NW = 4, NT = 256;
+    constexpr int SB = G::SB, PP = G::PP, RB = G::RB, RT = G::RT, DY = G::DY, KS = G::KS;
+    constexpr int SL = BITS == 4 ? 4 : (BITS == 2 ? 6 : 0);  // log2 of the weight scale
+    constexpr int UPF = 2;                                    // prefetched 16-byte quads per thread
+    constexpr int WROW = KH * KW * P;                         // packed bytes per filter bank
+    extern __shared__ __align__(16) uint8_t smem[];
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, r32 = lane & 31, h = lane >> 5;
+    const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+    const int gy = blockIdx.y;
+    const int ch = gy * 32 + r32;
+    const bool live = ch < a.m;
+    const int npix = a.h * a.w_;
+    const int imgq = npix * P / 16;  // 16-byte quads per image (P = 4: with a.quads)
+
+    // ---- the first image group's bytes: issued before anything else ----
+    uint4 pf[UPF];
+    auto issue = [&](int grp) {
+        const int i0 = grp * a.ipw;
+        const int ni = min(a.ipw, a.n - i0);
+        const uint8_t *src = a.x + (size_t)i0 * npix * P;
+#pragma unroll
+        for (int u = 0; u < UPF; ++u) {
+            const int q = tid + u * NT;
+            pf[u] = make_uint4(0, 0, 0, 0);
+            if (a.quads) {
+                if (q < ni * imgq)
+                    pf[u] = *(const uint4 *)(src + (size_t)q * 16);
+            } else {
+                // one-word pixels, npix not a multiple of 4 (a single image per step)
+                const uint32_t *s4 = (const uint32_t *)src;
+                if (4 * q < npix)
+                    pf[u].x = s4[4 * q];
+                if (4 * q + 1 < npix)
+                    pf[u].y = s4[4 * q + 1];
+                if (4 * q + 2 < npix)
+                    pf[u].z = s4[4 * q + 2];
+                if (4 * q + 3 < npix)
+                    pf[u].w = s4[4 * q + 3];
+            }
+        }
+    };
+    int grp = blockIdx.x;
+    if (grp < a.ngroups)
+        issue(grp);
+
+    // ---- filters: the lane's fragment of every K step, expanded to int8
+    // (4-/2-bit weights as 16*w / 64*w) ----
+    v4i A[KS];
+    int wsum = 0;
+    {
+        const uint8_t *wb = a.w + (size_t)(live ? ch : 0) * WROW;
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            uint32_t d[4];
+            if constexpr (G::CHUNK) {
+                // tap t, unpacked bytes [32 j + 16 h, + 16): packed bytes
+                // [(32 j + 16 h) * BITS / 8, + 2 * BITS)
+                const int t = s / G::CPT, j = s % G::CPT;
+                const uint8_t *src = wb + t * P + (32 * j + 16 * h) * BITS / 8;
+                if (BITS == 8) {
+                    uint4 v = make_uint4(0, 0, 0, 0);
+                    if (live)
+                        v = *(const uint4 *)src;
+                    d[0] = v.x;
+                    d[1] = v.y;
+                    d[2] = v.z;
+                    d[3] = v.w;
+                } else if (BITS == 4) {
+                    uint2 v = make_uint2(0, 0);
+                    if (live)
+                        v = *(const uint2 *)src;
+                    const uint2 e0w = w4_word(v.x), e1w = w4_word(v.y);
+                    d[0] = e0w.x;
+                    d[1] = e0w.y;
+                    d[2] = e1w.x;
+                    d[3] = e1w.y;
+                } else {
+                    const uint4 e = w2_word(live ? *(const uint32_t *)src : 0u);
+                    d[0] = e.x;
+                    d[1] = e.y;
+                    d[2] = e.z;
+                    d[3] = e.w;
+                }
+            } else {
+                typedef typename G::BT TP;
+#pragma unroll
+                for (int t = 0; t < G::TPF; ++t) {
+                    const int tp = TP::tap(s * G::TPF + t);
+                    const int ky = (tp >> 8) + h * DY, kx = tp & 255;
+                    uint32_t v = 0;
+                    if (tp >= 0 && live && ky < KH)
+                        v = *(const uint32_t *)(wb + (ky * KW + kx) * 4);
+                    if (BITS == 8) {
+                        d[t] = v;
+                    } else if (BITS == 4) {
+                        const uint2 e = w4_word(v);
+                        d[2 * t] = e.x;
+                        d[2 * t + 1] = e.y;
+                    } else {
+                        const uint4 e = w2_word(v);
+                        d[0] = e.x;
+                        d[1] = e.y;
+                        d[2] = e.z;
+                        d[3] = e.w;
+                    }
+                }
+            }
+            if (BITS == 8) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    wsum += (int)(int8_t)d[i] + (int)(int8_t)(d[i] >> 8) + (int)(int8_t)(d[i] >> 16) +
+                            (int)(int8_t)(d[i] >> 24);
+            }
+            A[s] = (v4i){(int32_t)d[0], (int32_t)d[1], (int32_t)d[2], (int32_t)d[3]};
+        }
+    }
+    if (BITS == 8)
+        wsum += __shfl_xor(wsum, 32, 64);  // the other lane half's share of the channel
+
+    // ---- the channel's compression plan (requant_plan) ----
+    int32_t p_bias = 0, p_mult = 0, p_shift = 0;
+    if (live) {
+        if (a.bias)
+            p_bias = a.bias[ch];
+        if (a.epi == EPI_REQUANT) {
+            p_mult = a.mult[ch];
+            p_shift = a.shift[ch];
+        }
+    }
+    int4 e0, e1;
+    {
+        int64_t b = p_bias;
+        if (BITS == 8)
+            b += 128 * (int64_t)wsum;
+        const int sh = p_shift < 0 ? 0 : (p_shift > 62 ? 62 : p_shift);
+        requant_plan(b, p_mult, sh, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, SL, e0, e1);
+    }
+    // wave-uniform fast paths: every channel in the 32-bit strict form; in
+    // the 32- or 64-bit strict form; every channel's code non-decreasing in
+    // the accumulator (positive multiplier)
+    const bool all3 = __all(!live || e1.z == 3);
+    const bool all34 = __all(!live || e1.z == 3 || e1.z == 4);
+    const bool mono = __all(!live || e1.z != 0 || e0.z > 0);
+    const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);  // raw: bias (+ 128 wsum)
+
+    // ---- pads: every image tile holds the zero code once (staged: -128 at
+    // 8 bits); each image then overwrites only its interior ----
+    {
+        const uint32_t f = BITS == 8 ? 0x80808080u : 0u;
+        const uint4 f4 = make_uint4(f, f, f, f);
+        for (int i = tid; i < a.ipw * a.tile_bytes / 16; i += NT)
+            ((uint4 *)smem)[i] = f4;
+    }
+    __syncthreads();
+
+    const bool st_ok = live && (r32 % (8 / BITS)) == 0;
+    const int ch_byte = gy * 4 * BITS + ((r32 * BITS) >> 3);
+    // the lane's pixel in a row tile: image row T*RT + r32/WOP, column r32%WOP
+    const int lrow = r32 / WOP, lcol = r32 % WOP;
+    const int lane_slot = (lrow * PP + lcol) * SB + (G::CHUNK ? 16 * h : h * DY * RB);
+    for (; grp < a.ngroups; grp += gridDim.x) {
+        const int i0 = grp * a.ipw;
+        const int ni = min(a.ipw, a.n - i0);
+        // stage the prefetched bytes into the tile interiors
+#pragma unroll
+        for (int u = 0; u < UPF; ++u) {
+            const int q = tid + u * NT;
+            if (P == 4) {
+                // four one-word pixels per quad (one image per step when the
+                // image is not a whole number of quads)
+                const int ii = a.quads ? (int)fdiv((uint32_t)q, a.div_imgq) : 0;
+                const int p0 = 4 * (q - ii * imgq);
+                if (ii < ni && p0 < npix) {
+                    uint8_t *tile = smem + ii * a.tile_bytes;
+                    int iy = (int)fdiv((uint32_t)p0, a.div_w);
+                    int ix = p0 - iy * a.w_;
+                    const uint32_t wd[4] = {pf[u].x, pf[u].y, pf[u].z, pf[u].w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        if (p0 + j < npix) {
+                            uint8_t *dst = tile + ((iy + a.ph) * PP + ix + a.pw) * SB;
+                            stage_word<BITS>(dst, wd[j]);
+                            if (BITS == 8 && ix + a.pw > 0)
+                                stage_word<BITS>(dst - 4, wd[j]);  // second pixel of the slot on its left
+                        }
+                        if (++ix == a.w_) {
+                            ix = 0;
+                            ++iy;
+                        }
+                    }
+                }
+            } else {
+                // one quad is part of one pixel
+                const int ii = (int)fdiv((uint32_t)q, a.div_imgq);
+                const int qi = q - ii * imgq;
+                const int pix = (int)fdiv((uint32_t)qi, a.div_pq);
+                const int part = qi - pix * (P / 16);
+                if (ii < ni) {
+                    const int iy = (int)fdiv((uint32_t)pix, a.div_w);
+                    const int ix = pix - iy * a.w_;
+                    uint8_t *dst = smem + ii * a.tile_bytes + ((iy + a.ph) * PP + ix + a.pw) * SB + part * (16 * 8 / BITS);
+                    stage_word<BITS>(dst, pf[u].x);
+                    stage_word<BITS>(dst + 32 / BITS, pf[u].y);
+                    stage_word<BITS>(dst + 64 / BITS, pf[u].z);
+                    stage_word<BITS>(dst + 96 / BITS, pf[u].w);
+                }
+            }
+        }
+        __syncthreads();
+        if (grp + (int)gridDim.x < a.ngroups)
+            issue(grp + gridDim.x);
+
+        // work items: (image of the step, pair of row tiles), item = image *
+        // pairs + pair; wave wv takes items wv, wv + NW, ...
+        const int items = ni * a.pairs;
+        auto run = [&](auto epi) {
+            for (int it = wv; it < items; it += NW) {
+                const int ii = (int)fdiv((uint32_t)it, a.div_pairs);
+                const int tp = it - ii * a.pairs;
+                const uint8_t *p0 = smem + ii * a.tile_bytes + 2 * tp * RT * RB + lane_slot;
+                v16i c0, c1;
+                img_steps<BITS, P, KH, KW, WOP, 0>(p0, p0 + RT * RB, A, c0, c1);
+                epi(i0 + ii, tp, c0, c1);
+            }
+        };
+        // ---- epilogues: lane (r32, h) holds channel ch for tile pixels
+        // p = 8*(v/4) + 4h + v%4 (register v): image row T*RT + p/WOP,
+        // column p%WOP.  The form (every channel in the 32-bit or the 64-bit
+        // strict plan, or any plan) is chosen once per step, outside the
+        // tile loop.  Codes go straight to memory as bytes ----
+        if constexpr (POOL) {
+            typedef PoolWin<WOP> PW;
+            // pooled rows of the pair start at tp * 2*RT / 2
+            auto store_pool = [&](int img, int tp, const uint32_t *code) {
+                uint32_t byte[8];
+#pragma unroll
+                for (int k = 0; k < 8; ++k)
+                    byte[k] = img_pack_lanes<BITS>(code[k]);
+                if (!st_ok)
+                    return;
+                uint8_t *yb = a.y + (size_t)img * a.hp * a.wp * a.ypb + ch_byte;
+                if (a.ypb == 4 * BITS && a.wp == WOP / 2 && (tp + 1) * RT <= a.hp) {
+                    // one 32-channel group, whole pooled rows: compile-time strides
+                    constexpr int YP = 4 * BITS, WP = WOP / 2;
+                    uint8_t *yt = yb + ((size_t)tp * RT * WP + 2 * h) * YP;
+#pragma unroll
+                    for (int k = 0; k < 8; ++k)
+                        yt[(PW::prow(k) * WP + PW::pcol(k)) * YP] = (uint8_t)byte[k];
+                } else {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const int pr = tp * RT + PW::prow(k), pc = PW::pcol(k) + 2 * h;
+                        if (pr < a.hp && pc < a.wp)
+                            yb[((size_t)pr * a.wp + pc) * a.ypb] = (uint8_t)byte[k];
+                    }
+                }
+            };
+            auto win = [&](int k, const v16i &c0, const v16i &c1, int32_t &x0, int32_t &x1, int32_t &y0,
+                           int32_t &y1) {
+                const int v = PW::v0(k), d = PW::dv(k);
+                const v16i &ta = PW::t0(k) ? c1 : c0;
+                const v16i &tb = PW::t1(k) ? c1 : c0;
+                x0 = ta[v];
+                x1 = ta[v + 1];
+                y0 = tb[v + d];
+                y1 = tb[v + d + 1];
+            };
+            if (all3) {
+                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                    uint32_t code[8];
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        int32_t x0, x1, y0, y1;
+                        win(k, c0, c1, x0, x1, y0, y1);
+                        code[k] = img_code3(max(max(x0, x1), max(y0, y1)), e0, e1);
+                    }
+                    store_pool(img, tp, code);
+                });
+            } else if (all34) {
+                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                    uint32_t code[8];
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        int32_t x0, x1, y0, y1;
+                        win(k, c0, c1, x0, x1, y0, y1);
+                        code[k] = img_code4(max(max(x0, x1), max(y0, y1)), e0, e1);
+                    }
+                    store_pool(img, tp, code);
+                });
+            } else {
+                // rare forms (plans outside the strict form, or multipliers
+                // that are not positive): one pooled value at a time, kept
+                // rolled so their 64-bit temporaries do not crowd the
+                // registers of the fast forms
+                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                    uint8_t *yb = a.y + (size_t)img * a.hp * a.wp * a.ypb + ch_byte;
+#pragma unroll 1
+                    for (int k = 0; k < 8; ++k) {
+                        int32_t x0, x1, y0, y1;
+                        // the window's registers, selected at run time
+                        const int v = WOP == 32 ? 2 * k : (WOP == 16 ? 2 * (k & 3) : ((k & 2) << 2) + 2 * (k & 1));
+                        const int d = WOP == 32 ? 0 : (WOP == 16 ? 8 : 4);
+                        const bool sa = WOP == 32 ? false : (k >> 2) != 0;
+                        const bool sb = WOP == 32 ? true : (k >> 2) != 0;
+                        x0 = sa ? c1[v] : c0[v];
+                        x1 = sa ? c1[v + 1] : c0[v + 1];
+                        y0 = sb ? c1[v + d] : c0[v + d];
+                        y1 = sb ? c1[v + d + 1] : c0[v + d + 1];
+                        uint32_t code;
+                        if (mono)
+                            code = img_code<SL>(max(max(x0, x1), max(y0, y1)), e0, e1, a.clip_lo, a.clip_hi);
+                        else
+                            code = max(max(img_code<SL>(x0, e0, e1, a.clip_lo, a.clip_hi),
+                                           img_code<SL>(x1, e0, e1, a.clip_lo, a.clip_hi)),
+                                       max(img_code<SL>(y0, e0, e1, a.clip_lo, a.clip_hi),
+                                           img_code<SL>(y1, e0, e1, a.clip_lo, a.clip_hi)));
+                        const uint32_t byte = img_pack_lanes<BITS>(code);
+                        const int pr = tp * RT + (WOP == 32 ? 0 : (WOP == 16 ? k >> 2 : 2 * (k >> 2) + ((k >> 1) & 1)));
+                        const int pc = (WOP == 32 ? 4 * (k >> 1) + (k & 1)
+                                                  : (WOP == 16 ? 4 * ((k & 3) >> 1) + (k & 1) : (k & 1))) + 2 * h;
+                        if (st_ok && pr < a.hp && pc < a.wp)
+                            yb[((size_t)pr * a.wp + pc) * a.ypb] = (uint8_t)byte;
+                    }
+                });
+            }
+        } else if (a.epi == EPI_RAW32) {
+            run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                if (!live)
+                    return;
+#pragma unroll
+                for (int t = 0; t < 2; ++t) {
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int p = 8 * (v >> 2) + 4 * h + (v & 3);
+                        const int oy = (2 * tp + t) * RT + p / WOP, ox = p % WOP;
+                        const int32_t av = t ? c1[v] : c0[v];
+                        if (oy < a.ho && ox < a.wo)
+                            ((int32_t *)a.y)[(((size_t)img * a.ho + oy) * a.wo + ox) * a.m + ch] =
+                                (int32_t)(uint32_t)(uint64_t)((int64_t)(av >> SL) + bt);
+                    }
+                }
+            });
+        } else {
+            auto store_tiles = [&](int img, int tp, const uint32_t *code) {
+                uint32_t byte[32];
+#pragma unroll
+                for (int v = 0; v < 32; ++v)
+                    byte[v] = img_pack_lanes<BITS>(code[v]);
+                if (!st_ok)
+                    return;
+                uint8_t *yb = a.y + (size_t)img * a.ho * a.wo * a.ypb + ch_byte;
+                if (a.ypb == 4 * BITS && a.wo == WOP && (2 * tp + 2) * RT <= a.ho) {
+                    // one 32-channel group, whole rows: compile-time strides
+                    constexpr int YP = 4 * BITS;
+                    uint8_t *yt = yb + ((size_t)2 * tp * RT * WOP + 4 * h) * YP;
+#pragma unroll
+                    for (int v = 0; v < 32; ++v)
+                        yt[((v >> 4) * 32 + 8 * ((v & 15) >> 2) + (v & 3)) * YP] = (uint8_t)byte[v];
+                } else {
+#pragma unroll
+                    for (int v = 0; v < 32; ++v) {
+                        const int p = 8 * ((v & 15) >> 2) + 4 * h + (v & 3);
+                        const int oy = (2 * tp + (v >> 4)) * RT + p / WOP, ox = p % WOP;
+                        if (oy < a.ho && ox < a.wo)
+                            yb[((size_t)oy * a.wo + ox) * a.ypb] = (uint8_t)byte[v];
+                    }
+                }
+            };
+            if (all3) {
+                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                    uint32_t code[32];
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        code[v] = img_code3(c0[v], e0, e1);
+                        code[16 + v] = img_code3(c1[v], e0, e1);
+                    }
+                    store_tiles(img, tp, code);
+                });
+            } else if (all34) {
+                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                    uint32_t code[32];
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        code[v] = img_code4(c0[v], e0, e1);
+                        code[16 + v] = img_code4(c1[v], e0, e1);
+                    }
+                    store_tiles(img, tp, code);
+                });
+            } else {
+                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                    uint8_t *yb = a.y + (size_t)img * a.ho * a.wo * a.ypb + ch_byte;
+#pragma unroll
+                    for (int t = 0; t < 2; ++t) {
+#pragma unroll 1
+                        for (int v = 0; v < 16; ++v) {
+                            const uint32_t byte = img_pack_lanes<BITS>(
+                                img_code<SL>(t ? c1[v] : c0[v], e0, e1, a.clip_lo, a.clip_hi));
+                            const int p = 8 * (v >> 2) + 4 * h + (v & 3);
+                            const int oy = (2 * tp + t) * RT + p / WOP, ox = p % WOP;
+                            if (st_ok && oy < a.ho && ox < a.wo)
+                                yb[((size_t)oy * a.wo + ox) * a.ypb] = (uint8_t)byte;
+                        }
+                    }
+                });
+            }
+        }
+        __syncthreads();  // every wave is done with this step's tiles
+    }
+}
+
+// Grid: as many workgroups as the device holds at once (image groups each),
+// so no workgroup starts only after others have finished.
+template <typename K>
+hipError_t launch_img_grid(K kernel, const ImgArgs &a, int cus, hipStream_t s)
+{
+    const size_t lds = (size_t)a.ipw * a.tile_bytes;
+    int per_cu = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, lds) != hipSuccess || per_cu < 1)
+        per_cu = 1;
+    const int gy = (a.m + 31) / 32;
+    int64_t gx = ((int64_t)cus * per_cu + gy - 1) / gy;
+    if (gx > a.ngroups)
+        gx = a.ngroups;
+    if (gx < 1)
+        gx = 1;
+    hipLaunchKernelGGL(kernel, dim3((unsigned)gx, (unsigned)gy), dim3(256), lds, s, a);
+    return hipGetLastError();
+}
+
+template <int BITS, int P, int K, int WOP>
+hipError_t launch_img(const ImgArgs &a, int cus, hipStream_t s)
+{
+    if (a.pool)
+        return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, true>, a, cus, s);
+    return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, false>, a, cus, s);
+}
+
+}  // namespace qnn

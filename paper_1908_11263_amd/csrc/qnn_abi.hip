@@ -386,34 +386,69 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
     return QNN_ERR_UNSUPPORTED;
 }
 
-// One-word-pixel kernel (conv_px4_kernel): input pixels of exactly 4 packed
-// bytes, stride 1, 3x3 or 5x5 filters, output rows of at most 32 pixels,
-// images of at most 2048 pixels, scale-and-clamp (pooled or not) or raw
-// outputs, channel groups that fill whole output words, and an image tile
-// that fits 64 KB of LDS.  Fills everything but the
-// pointers and ypb; false when the layer does not qualify.
-bool plan_px4(Px4Args &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g, const qnn_epi *e,
-              int32_t ho, int32_t wo, bool pool)
+// Whole-image kernel (conv_img_kernel): stride 1, 3x3 or 5x5 filters, output
+// rows of at most 32 pixels, scale-and-clamp (pooled or not) or raw outputs,
+// channel groups that fill whole output words, and pixels of
+//   * 4 packed bytes (8, 4 or 2 bits: a network's first layer), or
+//   * 16 / 32 packed bytes whose unpacked pixel is a whole number of 32-byte
+//     chunks, with at most 28 K steps (filters held in registers);
+// a group of whole images per workgroup step (prefetched in at most 8 KB,
+// the tiles in at most 64 KB of LDS).  Fills everything but the pointers and
+// ypb; false when the layer does not qualify.
+bool plan_img(ImgArgs &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g, const qnn_epi *e,
+              int32_t ho, int32_t wo, bool pool, int &pbytes, int &wop)
 {
     const int bits = x->bits;
     if (bits != 8 && bits != 4 && bits != 2)
         return false;
-    if (pixel_bytes64(x) != 4 || g->stride_h != 1 || g->stride_w != 1)
+    const int64_t pb = pixel_bytes64(x);
+    if (g->stride_h != 1 || g->stride_w != 1)
         return false;
     if (!(g->kh == g->kw && (g->kh == 3 || g->kh == 5)))
         return false;
-    if (wo > 32 || (int64_t)x->h * x->w > 2048)
-        return false;
     if (!(e->kind == QNN_EPI_REQUANT || (e->kind == QNN_EPI_RAW32 && !pool)))
         return false;
-    if (((int64_t)m * bits) % 32 != 0)
+    if (((int64_t)m * bits) % 32 != 0 || wo > 32)
         return false;
-    const int sb = bits == 8 ? 8 : 32 / bits; // tile slot bytes (8 bits: a pixel pair)
-    const int pp = 32 + g->kw - 1;            // tile pitch, slots
-    const int dy = (g->kh + 1) / 2;           // filter rows per half band
-    const int64_t rows = 2 * (int64_t)((ho + 1) / 2) + 2 * dy - 1;
+    const int64_t u = pb * 8 / bits;  // unpacked bytes per pixel
+    const int taps = g->kh * g->kw;
+    if (pb == 4) {
+        wop = 32;
+    } else if (pb == 16 || pb == 32) {
+        if (u < 32 || taps * (u / 32) > 28)
+            return false;
+        // built: 16-byte pixels at 4 and 2 bits, 32-byte pixels at 8 and 4
+        // bits, 5x5 filters only with a single chunk per tap
+        if ((pb == 16 && bits == 8) || (pb == 32 && bits == 2))
+            return false;
+        wop = wo <= 8 ? 8 : (wo <= 16 ? 16 : 32);
+    } else {
+        return false;
+    }
+    pbytes = (int)pb;
+    const int64_t npix = (int64_t)x->h * x->w;
+    const int64_t img_bytes = npix * pb;
+    if (img_bytes > 8192)
+        return false;
+    const int sb = u == 4 ? 8 : (int)u;       // tile slot bytes (8-bit one-word pixels: a pair)
+    const int pp = wop + g->kw - 1;           // tile pitch, slots
+    const int rt = 32 / wop;                  // image rows per MFMA row tile
+    const int64_t tiles = (ho + rt - 1) / rt;
+    const int64_t pairs = (tiles + 1) / 2;
+    const int extra = u >= 32 ? g->kh - 1 : 2 * ((g->kh + 1) / 2) - 1;
+    const int64_t rows = 2 * pairs * rt + extra;
     const int64_t tile = (rows * pp * sb + 15) & ~(int64_t)15;
-    if (tile > 64 * 1024)
+    // images per step: enough row-tile pairs for the four waves, within the
+    // prefetch registers and 64 KB of LDS; several only when the step is a
+    // whole number of 16-byte quads
+    int64_t ipw = (4 + pairs - 1) / pairs;
+    if (ipw > 8192 / img_bytes)
+        ipw = 8192 / img_bytes;
+    if (ipw > (64 * 1024) / tile)
+        ipw = (64 * 1024) / tile;
+    if (img_bytes % 16 != 0)
+        ipw = 1;
+    if (ipw < 1)
         return false;
     memset(&p, 0, sizeof(p));
     p.bias = e->bias;
@@ -428,8 +463,14 @@ bool plan_px4(Px4Args &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g
     p.hp = ho / 2;
     p.wp = wo / 2;
     p.tile_bytes = (int32_t)tile;
-    p.quads = ((int64_t)x->h * x->w) % 4 == 0 ? 1 : 0;
+    p.ipw = (int32_t)ipw;
+    p.ngroups = (int32_t)((x->n + ipw - 1) / ipw);
+    p.pairs = (int32_t)pairs;
+    p.quads = img_bytes % 16 == 0 ? 1 : 0;
     p.div_w = make_fastdiv((uint32_t)x->w);
+    p.div_pairs = make_fastdiv((uint32_t)pairs);
+    p.div_imgq = make_fastdiv((uint32_t)(img_bytes / 16 > 0 ? img_bytes / 16 : 1));
+    p.div_pq = make_fastdiv((uint32_t)(pb >= 16 ? pb / 16 : 1));
     return true;
 }
 
@@ -527,23 +568,31 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
         return launch_conv_xnor(a, s) == hipSuccess ? QNN_OK : QNN_ERR_LAUNCH;
     }
 
-    // layers whose input pixel is one packed word (a network's first layer):
-    // the dedicated kernel, unless the caller forces another tile
-    const bool force_px4 = force && force->kernel == QNN_TILE_PX4;
-    if (!f4 && (!force || force_px4)) {
-        Px4Args p;
-        if (plan_px4(p, x, m, g, e, ho, wo, pool)) {
+    // small images (a network's first layer, or later layers of 8- to
+    // 32-pixel-wide images): the whole-image kernel, unless the caller
+    // forces another tile
+    const bool force_img = force && force->kernel == QNN_TILE_IMAGE;
+    if (!f4 && (!force || force_img)) {
+        ImgArgs p;
+        int pbytes = 0, wop = 0;
+        if (plan_img(p, x, m, g, e, ho, wo, pool, pbytes, wop)) {
             st = device_info(&cus);
             if (st != QNN_OK)
                 return st;
-            p.x = (const uint32_t *)x_dev;
+            p.x = (const uint8_t *)x_dev;
             p.w = (const uint8_t *)w_dev;
             p.y = (uint8_t *)y_dev;
             p.ypb = ypb;
-            return launch_conv_px4(p, x->bits, g->kh, g->kw, cus, s) == hipSuccess ? QNN_OK
-                                                                                 : QNN_ERR_LAUNCH;
+            hipError_t err;
+            if (pbytes == 4)
+                err = launch_conv_img_p4(p, x->bits, g->kh, cus, s);
+            else if (pbytes == 16)
+                err = launch_conv_img_p16(p, x->bits, g->kh, wop, cus, s);
+            else
+                err = launch_conv_img_p32(p, x->bits, g->kh, wop, cus, s);
+            return err == hipSuccess ? QNN_OK : QNN_ERR_LAUNCH;
         }
-        if (force_px4)
+        if (force_img)
             return QNN_ERR_UNSUPPORTED;
     }
 
@@ -756,7 +805,7 @@ qnn_status qnn_conv2d_tiled(const qnn_tensor *x, const void *x_dev, int32_t m, c
             return QNN_ERR_BITS;
         built = (tm == 0 && tn == 0 && tile->waves == 0) ||
                 ((tile->waves == 4 || tile->waves == 8) && (tn == 1 || tn == 2) && (tm == 1 || tm == 2));
-    } else if (tile->kernel == QNN_TILE_PX4) {
+    } else if (tile->kernel == QNN_TILE_IMAGE) {
         built = tm == 0 && tn == 0 && tile->waves == 0;
     } else if (tile->kernel == 16)
         built = tile->waves == 4 && (tm == 1 || tm == 2 || tm == 4) && (tn == 1 || tn == 2 || tn == 4);

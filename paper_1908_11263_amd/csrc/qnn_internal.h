@@ -78,22 +78,28 @@ struct ConvArgs {
     int32_t wunpack;       // 32x32 kernel: 4-/2-bit filters staged unpacked to int8
 };
 
-// Arguments of the one-word-pixel convolution (conv_px4_kernel): input
-// pixels of exactly 4 packed bytes, stride 1, output rows of at most 32
-// pixels; one workgroup walks whole images, one 32-channel group per
-// grid row.
-struct Px4Args {
-    const uint32_t *x;     // packed NHWC input, one word per pixel
-    const uint8_t *w;      // packed OHWI weights, one word per tap
+// Arguments of the whole-image convolution (conv_img_kernel): small images
+// (input pixels of 4, 16 or 32 packed bytes, output rows of at most 32
+// pixels), stride 1; a workgroup walks groups of whole images, one
+// 32-channel group per grid row.
+struct ImgArgs {
+    const uint8_t *x;      // packed NHWC input
+    const uint8_t *w;      // packed OHWI weights
     uint8_t *y;            // packed NHWC codes (pooled or not) or int32 [pix][M]
     const int32_t *bias, *mult;
     const int8_t *shift;
     int32_t n, h, w_, m, ph, pw, ho, wo;
     int32_t epi, clip_lo, clip_hi, ypb;
     int32_t pool, hp, wp;
-    int32_t tile_bytes;    // LDS bytes of the padded, unpacked image tile
-    int32_t quads;         // 1: the image is loaded as 16-byte quads (h*w % 4 == 0)
-    FastDiv div_w;
+    int32_t tile_bytes;    // LDS bytes of one padded, unpacked image tile
+    int32_t ipw;           // images per workgroup step
+    int32_t ngroups;       // ceil(n / ipw)
+    int32_t pairs;         // pairs of 32-pixel MFMA row tiles per image
+    int32_t quads;         // 1: an image step is loaded as 16-byte quads
+    FastDiv div_w;         // input width
+    FastDiv div_pairs;     // pairs
+    FastDiv div_imgq;      // 16-byte quads per image
+    FastDiv div_pq;        // 16-byte quads per pixel (pixels of 16 / 32 bytes)
 };
 
 // Arguments of the INT-1 XNOR/popcount convolution.
@@ -130,9 +136,11 @@ hipError_t launch_conv_m32_b2(const ConvArgs &a, int wm, int wn, int al16, int n
 hipError_t launch_conv_m32_f4(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_m32_f4b1(const ConvArgs &a, int wm, int wn, int al16, int nw, dim3 grid, hipStream_t s);
 hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s);
-// returns hipErrorInvalidValue for a (bits, kh, kw) with no built instance;
-// the grid fills the cus compute units with resident workgroups
-hipError_t launch_conv_px4(const Px4Args &a, int bits, int kh, int kw, int cus, hipStream_t s);
+// whole-image kernel; hipErrorInvalidValue for a shape with no built
+// instance; the grid fills the cus compute units with resident workgroups
+hipError_t launch_conv_img_p4(const ImgArgs &a, int bits, int k, int cus, hipStream_t s);
+hipError_t launch_conv_img_p16(const ImgArgs &a, int bits, int k, int wop, int cus, hipStream_t s);
+hipError_t launch_conv_img_p32(const ImgArgs &a, int bits, int k, int wop, int cus, hipStream_t s);
 hipError_t launch_maxpool(const PoolArgs &a, int bits, hipStream_t s);
 hipError_t launch_relu_s8(const uint8_t *x, uint8_t *y, size_t count, hipStream_t s);
 

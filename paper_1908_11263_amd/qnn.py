@@ -19,7 +19,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "qnn.h")
 
 EPI_REQUANT, EPI_THRESH1, EPI_RAW32, EPI_STAIR = 0, 1, 2, 3
 # qnn_tile.kernel values (include/qnn.h)
-TILE_MFMA16, TILE_MFMA32, TILE_FP4, TILE_PX4 = 16, 32, 4, 1
+TILE_MFMA16, TILE_MFMA32, TILE_FP4, TILE_IMAGE = 16, 32, 4, 1
 _EPI_NAMES = {"requant": EPI_REQUANT, "thresh1": EPI_THRESH1, "raw32": EPI_RAW32, "stair": EPI_STAIR}
 
 STATUS = {

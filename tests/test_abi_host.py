@@ -25,7 +25,7 @@ def test_exports_every_header_function(q, L):
     assert len(names) >= 12
     for name in names:
         assert hasattr(L, name), name
-    assert L.qnn_abi_version() == 6
+    assert L.qnn_abi_version() == 7
 
 
 def test_status_strings(q, L):
@@ -268,27 +268,37 @@ def test_conv_fp4_validation(q, L):
     assert call_conv_tiled(q, L, *big, (fp4, 0, 0, 0)) == 6
 
 
-def test_conv_px4_validation(q, L):
-    """The one-word-pixel kernel (QNN_TILE_PX4): only the (0, 0, 0) shape,
+def test_conv_image_validation(q, L):
+    """The whole-image kernel (QNN_TILE_IMAGE): only the (0, 0, 0) shape,
     only for layers it covers (refused on the host otherwise)."""
-    px4 = q.TILE_PX4
+    img = q.TILE_IMAGE
     REQ2 = (0, None, FAKE, FAKE, None, 0, 3)
+    REQ4 = (0, None, FAKE, FAKE, None, 0, 15)
     g5 = (5, 5, 1, 1, 2, 2)
+    g3 = (3, 3, 1, 1, 1, 1)
     ok8 = ((2, 32, 32, 4), 8, 32, g5, REQ8, (2, 32, 32, 32, 8))
-    assert call_conv_tiled(q, L, *ok8, (px4, 0, 0, 0)) == 8               # valid: no GPU here
-    assert call_conv_tiled(q, L, (2, 16, 16, 16), 2, 32, (3, 3, 1, 1, 1, 1), REQ2,
-                           (2, 16, 16, 32, 2), (px4, 0, 0, 0)) == 8
-    for tile in [(px4, 1, 0, 0), (px4, 0, 1, 0), (px4, 0, 0, 4)]:
+    assert call_conv_tiled(q, L, *ok8, (img, 0, 0, 0)) == 8               # valid: no GPU here
+    for args in [((2, 16, 16, 16), 2, 32, g3, REQ2, (2, 16, 16, 32, 2)),   # one-word pixels
+                 ((2, 16, 16, 32), 8, 32, g5, REQ8, (2, 16, 16, 32, 8)),   # 32-byte pixels, 5x5
+                 ((2, 8, 8, 32), 4, 64, g5, REQ4, (2, 8, 8, 64, 4)),       # 16-byte pixels, 8-wide
+                 ((1, 8, 30, 64), 4, 32, g3, REQ4, (1, 8, 30, 32, 4)),     # 32-byte pixels, 3x3
+                 ((1, 9, 16, 64), 2, 32, g3, REQ2, (1, 9, 16, 32, 2))]:    # 16-byte pixels at 2 bits
+        assert call_conv_tiled(q, L, *args, (img, 0, 0, 0)) == 8, args
+    for tile in [(img, 1, 0, 0), (img, 0, 1, 0), (img, 0, 0, 4)]:
         assert call_conv_tiled(q, L, *ok8, tile) == 4, tile               # not built
     refused = [
         ((1, 9, 9, 4), 8, 32, (3, 3, 2, 2, 1, 1), REQ8, (1, 5, 5, 32, 8)),     # stride 2
-        ((1, 9, 9, 8), 8, 32, (3, 3, 1, 1, 1, 1), REQ8, (1, 9, 9, 32, 8)),     # 8-byte pixels
-        ((1, 9, 40, 4), 8, 32, (3, 3, 1, 1, 1, 1), REQ8, (1, 9, 40, 32, 8)),   # 40 outputs per row
+        ((1, 9, 9, 8), 8, 32, g3, REQ8, (1, 9, 9, 32, 8)),                     # 8-byte pixels
+        ((1, 9, 9, 16), 8, 32, g3, REQ8, (1, 9, 9, 32, 8)),                    # 16-byte pixels at 8 bits
+        ((1, 9, 40, 4), 8, 32, g3, REQ8, (1, 9, 40, 32, 8)),                   # 40 outputs per row
         ((1, 9, 9, 4), 8, 32, (7, 7, 1, 1, 3, 3), REQ8, (1, 9, 9, 32, 8)),     # 7x7 filter
-        ((1, 9, 9, 16), 2, 24, (3, 3, 1, 1, 1, 1), REQ2, (1, 9, 9, 24, 2)),    # 48-bit output pixels
-        ((1, 65, 32, 4), 8, 32, (3, 3, 1, 1, 1, 1), REQ8, (1, 65, 32, 32, 8)),  # 2080 pixels
+        ((1, 9, 9, 16), 2, 24, g3, REQ2, (1, 9, 9, 24, 2)),                    # 48-bit output pixels
+        ((1, 65, 32, 4), 8, 32, g3, REQ8, (1, 65, 32, 32, 8)),                 # 8320-byte image
+        ((1, 9, 9, 64), 8, 32, g5, REQ8, (1, 9, 9, 32, 8)),                    # 5x5 of 64-byte pixels
+        ((1, 9, 9, 128), 2, 32, g3, REQ2, (1, 9, 9, 32, 2)),                   # 36 K steps
+        ((1, 17, 17, 32), 8, 32, g3, REQ8, (1, 17, 17, 32, 8)),                # 9248-byte image
     ]
     for args in refused:
-        assert call_conv_tiled(q, L, *args, (px4, 0, 0, 0)) == 7, args
-    assert call_conv_tiled(q, L, (1, 8, 8, 32), 1, 32, (3, 3, 1, 1, 1, 1),
-                           (1, None, None, None, FAKE, 0, 0), (1, 8, 8, 32, 1), (px4, 0, 0, 0)) == 4
+        assert call_conv_tiled(q, L, *args, (img, 0, 0, 0)) == 7, args
+    assert call_conv_tiled(q, L, (1, 8, 8, 32), 1, 32, g3,
+                           (1, None, None, None, FAKE, 0, 0), (1, 8, 8, 32, 1), (img, 0, 0, 0)) == 4

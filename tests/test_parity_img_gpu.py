@@ -1,10 +1,12 @@
-"""GPU parity of the one-word-pixel convolution kernel (QNN_TILE_PX4: layers
-whose input pixel is one packed 32-bit word, e.g. a network's first layer)
-against the CPU oracle, byte for byte: plain and pooled scale-and-clamp,
-raw accumulators, every compression-plan mode (including multipliers that
-are not positive, where pooling must follow the compression), odd and
-ragged image sizes, images loaded word by word, many images per
-workgroup, and layers the kernel must refuse."""
+"""GPU parity of the whole-image convolution kernel (QNN_TILE_IMAGE: small
+images whose padded tiles fit in local memory -- a network's first layer
+with one-word pixels, and layers of 8- to 32-pixel-wide images with 16- or
+32-byte pixels) against the CPU oracle, byte for byte: plain and pooled
+scale-and-clamp, raw accumulators, every compression-plan mode (including
+multipliers that are not positive, where pooling must follow the
+compression), odd and ragged image sizes, images loaded word by word,
+several images per workgroup step, many steps per workgroup, and layers
+the kernel must refuse."""
 import numpy as np
 import pytest
 
@@ -13,7 +15,7 @@ from gpu_helpers import EPI, dev, log, oracle_conv, threads
 
 pytestmark = pytest.mark.gpu
 
-PX4 = (1, 0, 0, 0)
+IMAGE = (1, 0, 0, 0)
 
 
 @pytest.fixture(scope="module")
@@ -27,12 +29,12 @@ def qnn():
 
 
 def layer(bits, n, h, w, m, k, pad, seed, epi="requant", mult_rng=(1, 1 << 10), shift=10,
-          clip=None):
-    """One-word pixels: 32/bits channels."""
+          clip=None, c=None):
+    """One-word pixels (32/bits channels) unless c is given."""
     hi = (1 << bits) - 1
     whi = (1 << (bits - 1)) - 1
-    c = 32 // bits
-    return synth.conv_layer("px4_int%d" % bits, bits, n, h, w, c, m, k, pad, seed, (0, hi),
+    c = c or 32 // bits
+    return synth.conv_layer("img_int%d_c%d" % (bits, c), bits, n, h, w, c, m, k, pad, seed, (0, hi),
                             (-(1 << (bits - 1)), whi), bias_rng=(-hi * 50, hi * 50),
                             mult_rng=mult_rng, shift=shift, clip=clip or (0, hi), epi=epi)
 
@@ -84,7 +86,7 @@ SHAPES = [
 
 @pytest.mark.parametrize("bits", [8, 4, 2])
 @pytest.mark.parametrize("pool", [False, True])
-def test_px4_requant(qnn, orc, bits, pool):
+def test_img_requant(qnn, orc, bits, pool):
     for i, (n, h, w, m, k, pad) in enumerate(SHAPES):
         if m * bits % 32:
             continue
@@ -94,11 +96,11 @@ def test_px4_requant(qnn, orc, bits, pool):
         check(qnn, orc, L, pool=pool)
         if not pool:
             # the library's choice is this kernel: forcing it gives the same bytes
-            check(qnn, orc, L, tile=PX4)
+            check(qnn, orc, L, tile=IMAGE)
 
 
 @pytest.mark.parametrize("bits", [8, 4, 2])
-def test_px4_raw32(qnn, orc, bits):
+def test_img_raw32(qnn, orc, bits):
     for i, (n, h, w, m, k, pad) in enumerate(SHAPES):
         if m * bits % 32:
             continue
@@ -106,7 +108,7 @@ def test_px4_raw32(qnn, orc, bits):
 
 
 @pytest.mark.parametrize("bits", [8, 4, 2])
-def test_px4_plan_modes(qnn, orc, bits):
+def test_img_plan_modes(qnn, orc, bits):
     """Multipliers above 2^shift (the general plan forms), shift 0 and clip
     bounds inside the code range, and multipliers that are zero or negative
     (the compression is not monotone: codes are pooled after it)."""
@@ -122,44 +124,47 @@ def test_px4_plan_modes(qnn, orc, bits):
 
 
 @pytest.mark.parametrize("bits", [8, 4])
-def test_px4_many_images(qnn, orc, bits):
+def test_img_many_images(qnn, orc, bits):
     """More images than workgroups: every workgroup walks several images
     with the next image's words prefetched."""
     L = layer(bits, 2500, 16, 16, 32, 3, 1, seed=bits)
     check(qnn, orc, L, pool=True)
 
 
-def test_px4_equals_general_kernels(qnn, orc):
+def test_img_equals_general_kernels(qnn, orc):
     """The same layer through the one-word-pixel kernel and through the
     general 32x32 and 16x16 tiles."""
     for bits in (8, 4, 2):
         L = layer(bits, 2, 32, 32, 32, 5, 2, seed=bits)
         ref = want(orc, L)
-        for tile in (PX4, (32, 1, 2, 4), (16, 2, 1, 4)):
+        for tile in (IMAGE, (32, 1, 2, 4), (16, 2, 1, 4)):
             assert np.array_equal(run(qnn, L, tile=tile), ref), (bits, tile)
 
 
-def test_px4_refuses_layers_it_does_not_cover(qnn, orc):
+def test_img_refuses_layers_it_does_not_cover(qnn, orc):
     """Forced on a layer outside its domain the kernel is refused with
     QNN_ERR_UNSUPPORTED (7); the library's own choice still matches."""
     L8 = layer(8, 1, 9, 9, 32, 3, 1, seed=1)
     outside = [
-        synth.conv_layer("px4_stride2", 8, 1, 9, 9, 4, 32, 3, 1, 2, (0, 255), (-128, 127),
+        synth.conv_layer("img_stride2", 8, 1, 9, 9, 4, 32, 3, 1, 2, (0, 255), (-128, 127),
                          bias_rng=(-99, 99), mult_rng=(1, 1 << 10), shift=10, clip=(0, 255),
                          stride=2),                                        # stride 2
-        synth.conv_layer("px4_c8", 8, 1, 9, 9, 8, 32, 3, 1, 2, (0, 255), (-128, 127),
+        synth.conv_layer("img_c8", 8, 1, 9, 9, 8, 32, 3, 1, 2, (0, 255), (-128, 127),
                          bias_rng=(-99, 99), mult_rng=(1, 1 << 10), shift=10, clip=(0, 255)),  # 8-byte pixels
+        layer(8, 1, 9, 9, 32, 5, 2, seed=5, c=64),                         # 5x5, 64-byte pixels
+        layer(4, 1, 9, 9, 32, 5, 2, seed=6, c=64),                         # 5x5, 2 chunks per tap
+        layer(2, 1, 9, 9, 32, 3, 1, seed=7, c=128),                        # 3x3, 4 chunks per tap
         layer(8, 1, 9, 40, 32, 3, 1, seed=2),                              # rows of 40 outputs
         layer(8, 1, 9, 9, 32, 1, 0, seed=3),                               # 1x1 filter
         layer(2, 1, 9, 9, 24, 3, 1, seed=4),                               # 24 channels at 2 bits
     ]
     for L in outside:
         with pytest.raises(qnn.QnnError) as e:
-            run(qnn, L, tile=PX4)
+            run(qnn, L, tile=IMAGE)
         assert e.value.status == 7, L.name
         check(qnn, orc, L)
     with pytest.raises(qnn.QnnError) as e:
-        run(qnn, with_stair(L8), tile=PX4)
+        run(qnn, with_stair(L8), tile=IMAGE)
     assert e.value.status in (2, 7)
 
 
@@ -167,3 +172,55 @@ def with_stair(L):
     return synth.ConvLayer(L.name + "_stair", L.bits, L.n, L.h, L.w, L.c, L.m, L.kh, L.kw,
                            L.stride, L.pad, "stair", L.x_vals, L.w_vals, L.bias, None, None,
                            np.zeros((L.m, (1 << L.bits) - 1), np.int32), L.clip, L.c_alg)
+
+
+# (bits, channels, n, h, w, m, k, pad): 16- and 32-byte pixels, output rows
+# of 8, 16 and up to 32 pixels, ragged sizes, several 32-channel groups, and
+# the CIFAR-shaped network's second and third layers
+WIDE = [
+    (8, 32, 3, 16, 16, 32, 5, 2),
+    (8, 32, 5, 8, 8, 64, 5, 2),
+    (8, 32, 2, 13, 11, 40, 3, 1),
+    (8, 32, 2, 7, 30, 32, 3, 1),
+    (8, 32, 1, 16, 16, 32, 3, 1),
+    (4, 32, 3, 16, 16, 32, 5, 2),
+    (4, 32, 6, 8, 8, 64, 5, 2),
+    (4, 64, 2, 12, 9, 24, 3, 1),
+    (4, 64, 2, 5, 26, 64, 3, 1),
+    (4, 32, 2, 21, 17, 48, 3, 0),
+    (2, 64, 3, 9, 16, 32, 3, 1),
+    (2, 64, 2, 6, 6, 48, 3, 2),
+]
+
+
+@pytest.mark.parametrize("pool", [False, True])
+def test_img_wide_pixels(qnn, orc, pool):
+    for i, (bits, c, n, h, w, m, k, pad) in enumerate(WIDE):
+        L = layer(bits, n, h, w, m, k, pad, seed=300 + i, c=c)
+        if pool and (L.ho < 2 or L.wo < 2):
+            continue
+        check(qnn, orc, L, pool=pool)
+        if not pool:
+            check(qnn, orc, L, tile=IMAGE)
+            check(qnn, orc, L, epi="raw32")
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_img_wide_plan_modes(qnn, orc, bits):
+    """The general plan forms and non-positive multipliers on 32-channel
+    16x16 and 8x8 images."""
+    hi = (1 << bits) - 1
+    for j, kw in enumerate([dict(mult_rng=(1 << 12, 1 << 14), shift=8),
+                            dict(mult_rng=(1, 3), shift=0, clip=(1, hi - 1)),
+                            dict(mult_rng=(-(1 << 10), 1 << 10), shift=9)]):
+        for (h, w) in ((16, 16), (8, 8)):
+            L = layer(bits, 3, h, w, 32, 5, 2, seed=70 + j, c=32, **kw)
+            check(qnn, orc, L)
+            check(qnn, orc, L, pool=True)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_img_wide_many_images(qnn, orc, bits):
+    """More image groups than workgroups, four 8x8 images per step."""
+    L = layer(bits, 3001, 8, 8, 64, 5, 2, seed=bits, c=32)
+    check(qnn, orc, L, pool=True)
