@@ -596,6 +596,17 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
             return QNN_ERR_UNSUPPORTED;
     }
 
+    // a filter covering the whole image with raw outputs (the network's
+    // classifier): the fully connected kernel, unless the caller forces a tile
+    if (!force && e->kind == QNN_EPI_RAW32 && x->bits != 1 && g->kh == x->h && g->kw == x->w &&
+        g->pad_h == 0 && g->pad_w == 0 && K % 64 == 0) {
+        st = device_info(&cus);
+        if (st != QNN_OK)
+            return st;
+        return launch_linear_raw((const uint8_t *)x_dev, (const uint8_t *)w_dev, e->bias, (int32_t *)y_dev,
+                                 x->n, m, (int32_t)K, x->bits, s) == hipSuccess ? QNN_OK : QNN_ERR_LAUNCH;
+    }
+
     ConvArgs a;
     memset(&a, 0, sizeof(a));
     a.x = (const uint8_t *)x_dev;

@@ -141,6 +141,9 @@ hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s);
 hipError_t launch_conv_img_p4(const ImgArgs &a, int bits, int k, int cus, hipStream_t s);
 hipError_t launch_conv_img_p16(const ImgArgs &a, int bits, int k, int wop, int cus, hipStream_t s);
 hipError_t launch_conv_img_p32(const ImgArgs &a, int bits, int k, int wop, int cus, hipStream_t s);
+// fully connected layer with raw outputs: K a multiple of 64 (linear.hip)
+hipError_t launch_linear_raw(const uint8_t *x, const uint8_t *w, const int32_t *bias, int32_t *y, int32_t n,
+                             int32_t m, int32_t k, int bits, hipStream_t s);
 hipError_t launch_maxpool(const PoolArgs &a, int bits, hipStream_t s);
 hipError_t launch_relu_s8(const uint8_t *x, uint8_t *y, size_t count, hipStream_t s);
 

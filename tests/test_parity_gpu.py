@@ -205,7 +205,10 @@ def test_deterministic_and_stream_independent(qnn, orc):
 def test_linear(qnn, orc, bits):
     import torch
     rng = np.random.default_rng(90 + bits)
-    for (n, h, w, c, m) in [(37, 4, 4, 64, 10), (5, 1, 1, 1024, 10), (9, 2, 3, 32 * 4 // bits, 33)]:
+    # K a multiple of 64 (the fully connected kernel) with ragged image and
+    # channel counts, and K = 96 at 8 bits (the convolution tiles)
+    for (n, h, w, c, m) in [(37, 4, 4, 64, 10), (5, 1, 1, 1024, 10), (9, 2, 3, 32 * 4 // bits, 33),
+                            (300, 4, 4, 128, 70), (16, 1, 1, 4096, 16), (33, 8, 8, 64, 1)]:
         if bits == 1:
             xv = 2 * rng.integers(0, 2, size=(n, h, w, c)) - 1
             wv = 2 * rng.integers(0, 2, size=(m, h * w * c)) - 1
