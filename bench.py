@@ -391,7 +391,7 @@ def main():
     traffic, kname = recorded_profile()
     roofline = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_INT8_TOPS,
                 "unit": "TOP/s", "frac": round(achieved / PEAK_INT8_TOPS, 5),
-                "traffic": traffic, "kernel": kname or "conv_m32_kernel (4-bit)",
+                "traffic": traffic, "kernel": kname or "conv_img_kernel<4, 32, 3, 3, 32, false, true> (row bands)",
                 "ops_per_launch": 2 * head_step.macs}
     out = {
         "metric": "GMAC/s per qconv layer at INT8/4/2/1 (batch), % of int8 MFMA peak",

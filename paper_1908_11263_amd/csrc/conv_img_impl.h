@@ -9,9 +9,14 @@
 //     whole images (several small images per step so that every wave has
 //     work): each padded image is staged once in LDS, unpacked to int8 (8-bit
 //     codes offset by -128, pads included); the next group's bytes are
-//     loaded into registers while the current one is computed.
+//     loaded into registers while the current one is computed.  Images too
+//     large for one tile (BAND) are walked in bands of output rows instead:
+//     a step stages the band's input rows plus the kh - 1 rows of its halo,
+//     rows above or below the image as pads.
 //   * The filters of the group live in registers for the whole kernel (one
-//     16-byte fragment per lane and K step), never in LDS.
+//     16-byte fragment per lane and K step); wide-pixel filters arrive
+//     through LDS once (coalesced loads of the group's rows, expanded to
+//     int8 there), and the group's compression plans are computed once.
 //   * A wave computes two MFMA row tiles of 32 output pixels at a time with
 //     v_mfma_i32_32x32x32_i8 (rows = pixels, columns = channels).  A row tile
 //     is 1, 2 or 4 output rows of an image WOP = 32, 16 or 8 pixels wide
@@ -84,6 +89,13 @@ struct ImgGeom {
     static constexpr int TPF = CHUNK ? 1 : BT::TPF;    // taps per fragment
     static constexpr int KS = CHUNK ? KH * KW * CPT : BT::NF;  // 32-deep K steps
     static constexpr int WB = CHUNK ? 16 * BITS / 8 : 4;  // packed filter bytes behind one fragment slot
+    // CHUNK filters pass through LDS unpacked: fragment unit u = 2 * (K
+    // step) + lane half of channel c at u * FP + 16 c (FP: one unit of all 32
+    // channels, padded); FLDS bytes in all.  XLDS: the LDS beyond the image
+    // tiles (filters, then 32 plans of 32 bytes and a vote word)
+    static constexpr int FP = 33 * 16;
+    static constexpr int FLDS = CHUNK ? 2 * KS * FP : 0;
+    static constexpr int XLDS = FLDS + 64 * 16 + 16;
 };
 
 // One 16-byte im2col fragment for K step S of the pixel whose tile slot is
@@ -219,6 +231,13 @@ __device__ __forceinline__ uint32_t img_pack_lanes(uint32_t code)
     return v;
 }
 
+// A compile-time int (the byte stride of an output pixel in the store fast
+// paths).
+template <int V>
+struct ImgConst {
+    static constexpr int value = V;
+};
+
 // 2x2 pooling windows of a pair of row tiles: window k (0..7) holds the
 // registers (tile, v) of its four outputs and its pooled row (relative to
 // the pair's first pooled row) and pooled column (without the lane half's
@@ -245,14 +264,15 @@ struct PoolWin {
     }
 };
 
-template <int BITS, int P, int KH, int KW, int WOP, bool POOL>
+template <int BITS, int P, int KH, int KW, int WOP, bool POOL, bool BAND>
 __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
 {
     typedef ImgGeom<BITS, P, KH, KW, WOP> G;
+    static_assert(!BAND || P >= 16, "row bands are built for pixels of whole 16-byte quads");
     constexpr int NW = 4, NT = 256;
     constexpr int SB = G::SB, PP = G::PP, RB = G::RB, RT = G::RT, DY = G::DY, KS = G::KS;
     constexpr int SL = BITS == 4 ? 4 : (BITS == 2 ? 6 : 0);  // log2 of the weight scale
-    constexpr int UPF = 2;                                    // prefetched 16-byte quads per thread
+    constexpr int UPF = BAND ? 3 : 2;                         // prefetched 16-byte quads per thread
     constexpr int WROW = KH * KW * P;                         // packed bytes per filter bank
     extern __shared__ __align__(16) uint8_t smem[];
     const int tid = threadIdx.x;
@@ -267,6 +287,23 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     // ---- the first image group's bytes: issued before anything else ----
     uint4 pf[UPF];
     auto issue = [&](int grp) {
+        if constexpr (BAND) {
+            // band of image img: tile row r is input row r0 + r; quads of
+            // rows outside the image stay zero (staged as the pad code)
+            const int img = (int)fdiv((uint32_t)grp, a.div_bands);
+            const int r0 = (grp - img * a.bands) * a.brows - a.ph;
+            const int rowq = a.w_ * (P / 16);
+            const int qlo = max(0, -r0) * rowq, qhi = min(a.trows, a.h - r0) * rowq;
+            const uint8_t *src = a.x + ((int64_t)img * a.h + r0) * a.w_ * P;
+#pragma unroll
+            for (int u = 0; u < UPF; ++u) {
+                const int q = tid + u * NT;
+                pf[u] = make_uint4(0, 0, 0, 0);
+                if (q >= qlo && q < qhi)
+                    pf[u] = *(const uint4 *)(src + (int64_t)q * 16);
+            }
+            return;
+        }
         const int i0 = grp * a.ipw;
         const int ni = min(a.ipw, a.n - i0);
         const uint8_t *src = a.x + (size_t)i0 * npix * P;
@@ -295,105 +332,120 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     if (grp < a.ngroups)
         issue(grp);
 
-    // ---- filters: the lane's fragment of every K step, expanded to int8
-    // (4-/2-bit weights as 16*w / 64*w) ----
+    // ---- filters: the lane's fragment of every K step as int8 (4-/2-bit
+    // weights as 16*w / 64*w) ----
+    // LDS behind the image tiles: the unpacked filter units (CHUNK), then the
+    // group's compression plans and fast-path votes
+    uint8_t *sF = smem + (size_t)a.ipw * a.tile_bytes;
+    int4 *sPlan = (int4 *)(sF + G::FLDS);  // [32 channels][e0, e1]
+    int *sVote = (int *)(sPlan + 64);
     v4i A[KS];
-    int wsum = 0;
-    {
+    if constexpr (G::CHUNK) {
+        // the fragment of K step s (tap s / CPT, chunk s % CPT) for lane half
+        // h is packed bytes [(2 s + h) * WB, + WB) of the channel's row: unit
+        // 2 s + h.  The group's 32 rows are contiguous: the workgroup loads
+        // them as 16-byte quads, expands every unit to 16 int8 values and
+        // stores unit u of channel c at u * FP + 16 c (units of missing
+        // channels are zero)
+        constexpr int WB = G::WB, FP = G::FP, QPR = WROW / 16, UPQ = 16 / WB;
+        const int nq = min(32, a.m - gy * 32) * QPR;
+        const uint8_t *wg = a.w + (size_t)gy * 32 * WROW;
+        for (int q = tid; q < 32 * QPR; q += NT) {
+            uint4 v = make_uint4(0, 0, 0, 0);
+            if (q < nq)
+                v = *(const uint4 *)(wg + (size_t)q * 16);
+            const int c = q / QPR;
+            uint8_t *dst = sF + (q - c * QPR) * UPQ * FP + c * 16;
+            if (BITS == 8) {
+                *(uint4 *)dst = v;
+            } else if (BITS == 4) {
+                const uint2 w0 = w4_word(v.x), w1 = w4_word(v.y), w2 = w4_word(v.z), w3 = w4_word(v.w);
+                *(uint4 *)dst = make_uint4(w0.x, w0.y, w1.x, w1.y);
+                *(uint4 *)(dst + FP) = make_uint4(w2.x, w2.y, w3.x, w3.y);
+            } else {
+                *(uint4 *)dst = w2_word(v.x);
+                *(uint4 *)(dst + FP) = w2_word(v.y);
+                *(uint4 *)(dst + 2 * FP) = w2_word(v.z);
+                *(uint4 *)(dst + 3 * FP) = w2_word(v.w);
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+            A[s] = *(const v4i *)(sF + (2 * s + h) * FP + r32 * 16);
+    } else {
         const uint8_t *wb = a.w + (size_t)(live ? ch : 0) * WROW;
+        typedef typename G::BT TP;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             uint32_t d[4];
-            if constexpr (G::CHUNK) {
-                // tap t, unpacked bytes [32 j + 16 h, + 16): packed bytes
-                // [(32 j + 16 h) * BITS / 8, + 2 * BITS)
-                const int t = s / G::CPT, j = s % G::CPT;
-                const uint8_t *src = wb + t * P + (32 * j + 16 * h) * BITS / 8;
+#pragma unroll
+            for (int t = 0; t < G::TPF; ++t) {
+                const int tp = TP::tap(s * G::TPF + t);
+                const int ky = (tp >> 8) + h * DY, kx = tp & 255;
+                uint32_t v = 0;
+                if (tp >= 0 && live && ky < KH)
+                    v = *(const uint32_t *)(wb + (ky * KW + kx) * 4);
                 if (BITS == 8) {
-                    uint4 v = make_uint4(0, 0, 0, 0);
-                    if (live)
-                        v = *(const uint4 *)src;
-                    d[0] = v.x;
-                    d[1] = v.y;
-                    d[2] = v.z;
-                    d[3] = v.w;
+                    d[t] = v;
                 } else if (BITS == 4) {
-                    uint2 v = make_uint2(0, 0);
-                    if (live)
-                        v = *(const uint2 *)src;
-                    const uint2 e0w = w4_word(v.x), e1w = w4_word(v.y);
-                    d[0] = e0w.x;
-                    d[1] = e0w.y;
-                    d[2] = e1w.x;
-                    d[3] = e1w.y;
+                    const uint2 e = w4_word(v);
+                    d[2 * t] = e.x;
+                    d[2 * t + 1] = e.y;
                 } else {
-                    const uint4 e = w2_word(live ? *(const uint32_t *)src : 0u);
+                    const uint4 e = w2_word(v);
                     d[0] = e.x;
                     d[1] = e.y;
                     d[2] = e.z;
                     d[3] = e.w;
                 }
-            } else {
-                typedef typename G::BT TP;
-#pragma unroll
-                for (int t = 0; t < G::TPF; ++t) {
-                    const int tp = TP::tap(s * G::TPF + t);
-                    const int ky = (tp >> 8) + h * DY, kx = tp & 255;
-                    uint32_t v = 0;
-                    if (tp >= 0 && live && ky < KH)
-                        v = *(const uint32_t *)(wb + (ky * KW + kx) * 4);
-                    if (BITS == 8) {
-                        d[t] = v;
-                    } else if (BITS == 4) {
-                        const uint2 e = w4_word(v);
-                        d[2 * t] = e.x;
-                        d[2 * t + 1] = e.y;
-                    } else {
-                        const uint4 e = w2_word(v);
-                        d[0] = e.x;
-                        d[1] = e.y;
-                        d[2] = e.z;
-                        d[3] = e.w;
-                    }
-                }
-            }
-            if (BITS == 8) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    wsum += (int)(int8_t)d[i] + (int)(int8_t)(d[i] >> 8) + (int)(int8_t)(d[i] >> 16) +
-                            (int)(int8_t)(d[i] >> 24);
             }
             A[s] = (v4i){(int32_t)d[0], (int32_t)d[1], (int32_t)d[2], (int32_t)d[3]};
         }
     }
-    if (BITS == 8)
-        wsum += __shfl_xor(wsum, 32, 64);  // the other lane half's share of the channel
 
-    // ---- the channel's compression plan (requant_plan) ----
-    int32_t p_bias = 0, p_mult = 0, p_shift = 0;
-    if (live) {
-        if (a.bias)
-            p_bias = a.bias[ch];
-        if (a.epi == EPI_REQUANT) {
-            p_mult = a.mult[ch];
-            p_shift = a.shift[ch];
+    // ---- the group's compression plans (requant_plan) and the wave-uniform
+    // fast paths: every channel in the 32-bit strict form; in the 32- or
+    // 64-bit strict form; every channel's code non-decreasing in the
+    // accumulator (positive multiplier).  Computed by wave 0 (whose lanes hold
+    // the same 32 channels as every wave's) and shared through LDS ----
+    if (wv == 0) {
+        int32_t wsum = 0;
+        if (BITS == 8) {
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t d = (uint32_t)A[s][i];
+                    wsum += (int)(int8_t)d + (int)(int8_t)(d >> 8) + (int)(int8_t)(d >> 16) + (int)(int8_t)(d >> 24);
+                }
+            wsum += __shfl_xor(wsum, 32, 64);  // the other lane half's share of the channel
         }
-    }
-    int4 e0, e1;
-    {
+        int32_t p_bias = 0, p_mult = 0, p_shift = 0;
+        if (live) {
+            if (a.bias)
+                p_bias = a.bias[ch];
+            if (a.epi == EPI_REQUANT) {
+                p_mult = a.mult[ch];
+                p_shift = a.shift[ch];
+            }
+        }
+        int4 q0, q1;
         int64_t b = p_bias;
         if (BITS == 8)
             b += 128 * (int64_t)wsum;
         const int sh = p_shift < 0 ? 0 : (p_shift > 62 ? 62 : p_shift);
-        requant_plan(b, p_mult, sh, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, SL, e0, e1);
+        requant_plan(b, p_mult, sh, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, SL, q0, q1);
+        const bool v3 = __all(!live || q1.z == 3);
+        const bool v34 = __all(!live || q1.z == 3 || q1.z == 4);
+        const bool vm = __all(!live || q1.z != 0 || q0.z > 0);
+        if (h == 0) {
+            sPlan[2 * r32] = q0;
+            sPlan[2 * r32 + 1] = q1;
+        }
+        if (lane == 0)
+            *sVote = (v3 ? 1 : 0) | (v34 ? 2 : 0) | (vm ? 4 : 0);
     }
-    // wave-uniform fast paths: every channel in the 32-bit strict form; in
-    // the 32- or 64-bit strict form; every channel's code non-decreasing in
-    // the accumulator (positive multiplier)
-    const bool all3 = __all(!live || e1.z == 3);
-    const bool all34 = __all(!live || e1.z == 3 || e1.z == 4);
-    const bool mono = __all(!live || e1.z != 0 || e0.z > 0);
-    const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);  // raw: bias (+ 128 wsum)
 
     // ---- pads: every image tile holds the zero code once (staged: -128 at
     // 8 bits); each image then overwrites only its interior ----
@@ -404,6 +456,10 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             ((uint4 *)smem)[i] = f4;
     }
     __syncthreads();
+    const int4 e0 = sPlan[2 * r32], e1 = sPlan[2 * r32 + 1];
+    const int votes = *sVote;
+    const bool all3 = (votes & 1) != 0, all34 = (votes & 2) != 0, mono = (votes & 4) != 0;
+    const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);  // raw: bias (+ 128 wsum)
 
     const bool st_ok = live && (r32 % (8 / BITS)) == 0;
     const int ch_byte = gy * 4 * BITS + ((r32 * BITS) >> 3);
@@ -411,8 +467,18 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     const int lrow = r32 / WOP, lcol = r32 % WOP;
     const int lane_slot = (lrow * PP + lcol) * SB + (G::CHUNK ? 16 * h : h * DY * RB);
     for (; grp < a.ngroups; grp += gridDim.x) {
-        const int i0 = grp * a.ipw;
-        const int ni = min(a.ipw, a.n - i0);
+        // the step's first image, its image count and the first output row
+        // of its tiles (non-zero for the later bands of an image)
+        int i0, ni, orow0;
+        if constexpr (BAND) {
+            i0 = (int)fdiv((uint32_t)grp, a.div_bands);
+            ni = 1;
+            orow0 = (grp - i0 * a.bands) * a.brows;
+        } else {
+            i0 = grp * a.ipw;
+            ni = min(a.ipw, a.n - i0);
+            orow0 = 0;
+        }
         // stage the prefetched bytes into the tile interiors
 #pragma unroll
         for (int u = 0; u < UPF; ++u) {
@@ -450,7 +516,10 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 if (ii < ni) {
                     const int iy = (int)fdiv((uint32_t)pix, a.div_w);
                     const int ix = pix - iy * a.w_;
-                    uint8_t *dst = smem + ii * a.tile_bytes + ((iy + a.ph) * PP + ix + a.pw) * SB + part * (16 * 8 / BITS);
+                    // whole images: interior rows below ph pad rows; bands:
+                    // every tile row staged (pads as zero quads)
+                    const int ty = BAND ? iy : iy + a.ph;
+                    uint8_t *dst = smem + ii * a.tile_bytes + (ty * PP + ix + a.pw) * SB + part * (16 * 8 / BITS);
                     stage_word<BITS>(dst, pf[u].x);
                     stage_word<BITS>(dst + 32 / BITS, pf[u].y);
                     stage_word<BITS>(dst + 64 / BITS, pf[u].z);
@@ -463,7 +532,8 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             issue(grp + gridDim.x);
 
         // work items: (image of the step, pair of row tiles), item = image *
-        // pairs + pair; wave wv takes items wv, wv + NW, ...
+        // pairs + pair; wave wv takes items wv, wv + NW, ...  The epilogue
+        // gets the pair's first output row (even).
         const int items = ni * a.pairs;
         auto run = [&](auto epi) {
             for (int it = wv; it < items; it += NW) {
@@ -472,7 +542,12 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 const uint8_t *p0 = smem + ii * a.tile_bytes + 2 * tp * RT * RB + lane_slot;
                 v16i c0, c1;
                 img_steps<BITS, P, KH, KW, WOP, 0>(p0, p0 + RT * RB, A, c0, c1);
-                epi(i0 + ii, tp, c0, c1);
+                // an opaque zero keeps the general paths' per-register bounds
+                // checks in this body (hoisted out of the loop they would hold
+                // a lane mask per output register throughout)
+                int ez = 0;
+                __asm__ volatile("" : "+v"(ez));
+                epi(i0 + ii, orow0 + 2 * tp * RT, ez, c0, c1);
             }
         };
         // ---- epilogues: lane (r32, h) holds channel ch for tile pixels
@@ -482,8 +557,8 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
         // tile loop.  Codes go straight to memory as bytes ----
         if constexpr (POOL) {
             typedef PoolWin<WOP> PW;
-            // pooled rows of the pair start at tp * 2*RT / 2
-            auto store_pool = [&](int img, int tp, const uint32_t *code) {
+            // pooled rows of the pair start at orow / 2
+            auto store_pool = [&](int img, int orow, int ez, const uint32_t *code) {
                 uint32_t byte[8];
 #pragma unroll
                 for (int k = 0; k < 8; ++k)
@@ -491,17 +566,24 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 if (!st_ok)
                     return;
                 uint8_t *yb = a.y + (size_t)img * a.hp * a.wp * a.ypb + ch_byte;
-                if (a.ypb == 4 * BITS && a.wp == WOP / 2 && (tp + 1) * RT <= a.hp) {
-                    // one 32-channel group, whole pooled rows: compile-time strides
-                    constexpr int YP = 4 * BITS, WP = WOP / 2;
-                    uint8_t *yt = yb + ((size_t)tp * RT * WP + 2 * h) * YP;
+                // whole pooled rows of pixels of one or two 32-channel
+                // groups: compile-time strides (immediate store offsets)
+                auto fast = [&](auto yp) {
+                    constexpr int YP = decltype(yp)::value, WP = WOP / 2;
+                    uint8_t *yt = yb + ((size_t)(orow >> 1) * WP + 2 * h) * YP;
 #pragma unroll
                     for (int k = 0; k < 8; ++k)
                         yt[(PW::prow(k) * WP + PW::pcol(k)) * YP] = (uint8_t)byte[k];
+                };
+                const bool rows = a.wp == WOP / 2 && (orow >> 1) + RT <= a.hp;
+                if (rows && a.ypb == 4 * BITS) {
+                    fast(ImgConst<4 * BITS>());
+                } else if (rows && a.ypb == 8 * BITS) {
+                    fast(ImgConst<8 * BITS>());
                 } else {
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
-                        const int pr = tp * RT + PW::prow(k), pc = PW::pcol(k) + 2 * h;
+                        const int pr = (orow >> 1) + PW::prow(k), pc = PW::pcol(k) + 2 * h + ez;
                         if (pr < a.hp && pc < a.wp)
                             yb[((size_t)pr * a.wp + pc) * a.ypb] = (uint8_t)byte[k];
                     }
@@ -518,7 +600,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 y1 = tb[v + d + 1];
             };
             if (all3) {
-                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
                     uint32_t code[8];
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
@@ -526,10 +608,10 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                         win(k, c0, c1, x0, x1, y0, y1);
                         code[k] = img_code3(max(max(x0, x1), max(y0, y1)), e0, e1);
                     }
-                    store_pool(img, tp, code);
+                    store_pool(img, orow, ez, code);
                 });
             } else if (all34) {
-                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
                     uint32_t code[8];
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
@@ -537,14 +619,14 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                         win(k, c0, c1, x0, x1, y0, y1);
                         code[k] = img_code4(max(max(x0, x1), max(y0, y1)), e0, e1);
                     }
-                    store_pool(img, tp, code);
+                    store_pool(img, orow, ez, code);
                 });
             } else {
                 // rare forms (plans outside the strict form, or multipliers
                 // that are not positive): one pooled value at a time, kept
                 // rolled so their 64-bit temporaries do not crowd the
                 // registers of the fast forms
-                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
                     uint8_t *yb = a.y + (size_t)img * a.hp * a.wp * a.ypb + ch_byte;
 #pragma unroll 1
                     for (int k = 0; k < 8; ++k) {
@@ -567,24 +649,24 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                                        max(img_code<SL>(y0, e0, e1, a.clip_lo, a.clip_hi),
                                            img_code<SL>(y1, e0, e1, a.clip_lo, a.clip_hi)));
                         const uint32_t byte = img_pack_lanes<BITS>(code);
-                        const int pr = tp * RT + (WOP == 32 ? 0 : (WOP == 16 ? k >> 2 : 2 * (k >> 2) + ((k >> 1) & 1)));
+                        const int pr = (orow >> 1) + (WOP == 32 ? 0 : (WOP == 16 ? k >> 2 : 2 * (k >> 2) + ((k >> 1) & 1)));
                         const int pc = (WOP == 32 ? 4 * (k >> 1) + (k & 1)
-                                                  : (WOP == 16 ? 4 * ((k & 3) >> 1) + (k & 1) : (k & 1))) + 2 * h;
+                                                  : (WOP == 16 ? 4 * ((k & 3) >> 1) + (k & 1) : (k & 1))) + 2 * h + ez;
                         if (st_ok && pr < a.hp && pc < a.wp)
                             yb[((size_t)pr * a.wp + pc) * a.ypb] = (uint8_t)byte;
                     }
                 });
             }
         } else if (a.epi == EPI_RAW32) {
-            run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+            run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
                 if (!live)
                     return;
 #pragma unroll
                 for (int t = 0; t < 2; ++t) {
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
-                        const int p = 8 * (v >> 2) + 4 * h + (v & 3);
-                        const int oy = (2 * tp + t) * RT + p / WOP, ox = p % WOP;
+                        const int p = 8 * (v >> 2) + 4 * h + (v & 3) + ez;
+                        const int oy = orow + t * RT + p / WOP, ox = p % WOP;
                         const int32_t av = t ? c1[v] : c0[v];
                         if (oy < a.ho && ox < a.wo)
                             ((int32_t *)a.y)[(((size_t)img * a.ho + oy) * a.wo + ox) * a.m + ch] =
@@ -593,7 +675,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 }
             });
         } else {
-            auto store_tiles = [&](int img, int tp, const uint32_t *code) {
+            auto store_tiles = [&](int img, int orow, int ez, const uint32_t *code) {
                 uint32_t byte[32];
 #pragma unroll
                 for (int v = 0; v < 32; ++v)
@@ -601,45 +683,52 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 if (!st_ok)
                     return;
                 uint8_t *yb = a.y + (size_t)img * a.ho * a.wo * a.ypb + ch_byte;
-                if (a.ypb == 4 * BITS && a.wo == WOP && (2 * tp + 2) * RT <= a.ho) {
-                    // one 32-channel group, whole rows: compile-time strides
-                    constexpr int YP = 4 * BITS;
-                    uint8_t *yt = yb + ((size_t)2 * tp * RT * WOP + 4 * h) * YP;
+                // whole rows of pixels of one or two 32-channel groups:
+                // compile-time strides (immediate store offsets)
+                auto fast = [&](auto yp) {
+                    constexpr int YP = decltype(yp)::value;
+                    uint8_t *yt = yb + ((size_t)orow * WOP + 4 * h) * YP;
 #pragma unroll
                     for (int v = 0; v < 32; ++v)
                         yt[((v >> 4) * 32 + 8 * ((v & 15) >> 2) + (v & 3)) * YP] = (uint8_t)byte[v];
+                };
+                const bool rows = a.wo == WOP && orow + 2 * RT <= a.ho;
+                if (rows && a.ypb == 4 * BITS) {
+                    fast(ImgConst<4 * BITS>());
+                } else if (rows && a.ypb == 8 * BITS) {
+                    fast(ImgConst<8 * BITS>());
                 } else {
 #pragma unroll
                     for (int v = 0; v < 32; ++v) {
-                        const int p = 8 * ((v & 15) >> 2) + 4 * h + (v & 3);
-                        const int oy = (2 * tp + (v >> 4)) * RT + p / WOP, ox = p % WOP;
+                        const int p = 8 * ((v & 15) >> 2) + 4 * h + (v & 3) + ez;
+                        const int oy = orow + (v >> 4) * RT + p / WOP, ox = p % WOP;
                         if (oy < a.ho && ox < a.wo)
                             yb[((size_t)oy * a.wo + ox) * a.ypb] = (uint8_t)byte[v];
                     }
                 }
             };
             if (all3) {
-                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
                     uint32_t code[32];
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
                         code[v] = img_code3(c0[v], e0, e1);
                         code[16 + v] = img_code3(c1[v], e0, e1);
                     }
-                    store_tiles(img, tp, code);
+                    store_tiles(img, orow, ez, code);
                 });
             } else if (all34) {
-                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
                     uint32_t code[32];
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
                         code[v] = img_code4(c0[v], e0, e1);
                         code[16 + v] = img_code4(c1[v], e0, e1);
                     }
-                    store_tiles(img, tp, code);
+                    store_tiles(img, orow, ez, code);
                 });
             } else {
-                run([&](int img, int tp, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
                     uint8_t *yb = a.y + (size_t)img * a.ho * a.wo * a.ypb + ch_byte;
 #pragma unroll
                     for (int t = 0; t < 2; ++t) {
@@ -647,8 +736,8 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                         for (int v = 0; v < 16; ++v) {
                             const uint32_t byte = img_pack_lanes<BITS>(
                                 img_code<SL>(t ? c1[v] : c0[v], e0, e1, a.clip_lo, a.clip_hi));
-                            const int p = 8 * (v >> 2) + 4 * h + (v & 3);
-                            const int oy = (2 * tp + t) * RT + p / WOP, ox = p % WOP;
+                            const int p = 8 * (v >> 2) + 4 * h + (v & 3) + ez;
+                            const int oy = orow + t * RT + p / WOP, ox = p % WOP;
                             if (st_ok && oy < a.ho && ox < a.wo)
                                 yb[((size_t)oy * a.wo + ox) * a.ypb] = (uint8_t)byte;
                         }
@@ -663,9 +752,9 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
 // Grid: as many workgroups as the device holds at once (image groups each),
 // so no workgroup starts only after others have finished.
 template <typename K>
-hipError_t launch_img_grid(K kernel, const ImgArgs &a, int cus, hipStream_t s)
+hipError_t launch_img_grid(K kernel, const ImgArgs &a, int flds, int cus, hipStream_t s)
 {
-    const size_t lds = (size_t)a.ipw * a.tile_bytes;
+    const size_t lds = (size_t)a.ipw * a.tile_bytes + flds;
     int per_cu = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 256, lds) != hipSuccess || per_cu < 1)
         per_cu = 1;
@@ -679,12 +768,13 @@ hipError_t launch_img_grid(K kernel, const ImgArgs &a, int cus, hipStream_t s)
     return hipGetLastError();
 }
 
-template <int BITS, int P, int K, int WOP>
+template <int BITS, int P, int K, int WOP, bool BAND = false>
 hipError_t launch_img(const ImgArgs &a, int cus, hipStream_t s)
 {
+    constexpr int FLDS = ImgGeom<BITS, P, K, K, WOP>::XLDS;
     if (a.pool)
-        return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, true>, a, cus, s);
-    return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, false>, a, cus, s);
+        return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, true, BAND>, a, FLDS, cus, s);
+    return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, false, BAND>, a, FLDS, cus, s);
 }
 
 }  // namespace qnn

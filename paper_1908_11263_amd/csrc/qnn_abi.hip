@@ -393,8 +393,10 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
 //   * 16 / 32 packed bytes whose unpacked pixel is a whole number of 32-byte
 //     chunks, with at most 28 K steps (filters held in registers);
 // a group of whole images per workgroup step (prefetched in at most 8 KB,
-// the tiles in at most 64 KB of LDS).  Fills everything but the pointers and
-// ypb; false when the layer does not qualify.
+// the tiles in at most 64 KB of LDS), or, for larger images of 32-byte
+// pixels and rows of 17 to 32 outputs, one band of 8 output rows per step
+// (its kh + 7 input rows prefetched in at most 12 KB).  Fills everything but
+// the pointers and ypb; false when the layer does not qualify.
 bool plan_img(ImgArgs &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g, const qnn_epi *e,
               int32_t ho, int32_t wo, bool pool, int &pbytes, int &wop)
 {
@@ -428,11 +430,45 @@ bool plan_img(ImgArgs &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g
     pbytes = (int)pb;
     const int64_t npix = (int64_t)x->h * x->w;
     const int64_t img_bytes = npix * pb;
-    if (img_bytes > 8192)
-        return false;
     const int sb = u == 4 ? 8 : (int)u;       // tile slot bytes (8-bit one-word pixels: a pair)
     const int pp = wop + g->kw - 1;           // tile pitch, slots
     const int rt = 32 / wop;                  // image rows per MFMA row tile
+    if (img_bytes > 8192) {
+        // row bands: built for 32-byte pixels with 32-pixel row tiles
+        if (!(pb == 32 && wop == 32))
+            return false;
+        const int brows = 2 * rt * 4;         // a pair of row tiles per wave
+        const int trows = brows + g->kh - 1;
+        const int64_t bands = (ho + brows - 1) / brows;
+        if ((int64_t)trows * x->w * pb > 3 * 256 * 16 || (int64_t)x->n * bands > INT32_MAX)
+            return false;
+        memset(&p, 0, sizeof(p));
+        p.bias = e->bias;
+        p.mult = e->mult;
+        p.shift = e->shift;
+        p.n = x->n; p.h = x->h; p.w_ = x->w; p.m = m;
+        p.ph = g->pad_h; p.pw = g->pad_w; p.ho = ho; p.wo = wo;
+        p.epi = e->kind;
+        p.clip_lo = e->clip_lo;
+        p.clip_hi = e->clip_hi;
+        p.pool = pool ? 1 : 0;
+        p.hp = ho / 2;
+        p.wp = wo / 2;
+        p.tile_bytes = (int32_t)(((int64_t)trows * pp * sb + 15) & ~(int64_t)15);
+        p.ipw = 1;
+        p.ngroups = (int32_t)(x->n * bands);
+        p.pairs = brows / (2 * rt);
+        p.quads = 1;
+        p.div_w = make_fastdiv((uint32_t)x->w);
+        p.div_pairs = make_fastdiv((uint32_t)p.pairs);
+        p.div_imgq = make_fastdiv((uint32_t)(trows * x->w * pb / 16));
+        p.div_pq = make_fastdiv((uint32_t)(pb / 16));
+        p.bands = (int32_t)bands;
+        p.brows = brows;
+        p.trows = trows;
+        p.div_bands = make_fastdiv((uint32_t)bands);
+        return true;
+    }
     const int64_t tiles = (ho + rt - 1) / rt;
     const int64_t pairs = (tiles + 1) / 2;
     const int extra = u >= 32 ? g->kh - 1 : 2 * ((g->kh + 1) / 2) - 1;

@@ -282,7 +282,9 @@ def test_conv_image_validation(q, L):
                  ((2, 16, 16, 32), 8, 32, g5, REQ8, (2, 16, 16, 32, 8)),   # 32-byte pixels, 5x5
                  ((2, 8, 8, 32), 4, 64, g5, REQ4, (2, 8, 8, 64, 4)),       # 16-byte pixels, 8-wide
                  ((1, 8, 30, 64), 4, 32, g3, REQ4, (1, 8, 30, 32, 4)),     # 32-byte pixels, 3x3
-                 ((1, 9, 16, 64), 2, 32, g3, REQ2, (1, 9, 16, 32, 2))]:    # 16-byte pixels at 2 bits
+                 ((1, 9, 16, 64), 2, 32, g3, REQ2, (1, 9, 16, 32, 2)),     # 16-byte pixels at 2 bits
+                 ((1, 17, 17, 32), 8, 32, g3, REQ8, (1, 17, 17, 32, 8)),   # 9248-byte image: row bands
+                 ((2, 32, 32, 64), 4, 64, g3, REQ4, (2, 32, 32, 64, 4))]:  # row bands, 2 channel groups
         assert call_conv_tiled(q, L, *args, (img, 0, 0, 0)) == 8, args
     for tile in [(img, 1, 0, 0), (img, 0, 1, 0), (img, 0, 0, 4)]:
         assert call_conv_tiled(q, L, *ok8, tile) == 4, tile               # not built
@@ -296,7 +298,8 @@ def test_conv_image_validation(q, L):
         ((1, 65, 32, 4), 8, 32, g3, REQ8, (1, 65, 32, 32, 8)),                 # 8320-byte image
         ((1, 9, 9, 64), 8, 32, g5, REQ8, (1, 9, 9, 32, 8)),                    # 5x5 of 64-byte pixels
         ((1, 9, 9, 128), 2, 32, g3, REQ2, (1, 9, 9, 32, 2)),                   # 36 K steps
-        ((1, 17, 17, 32), 8, 32, g3, REQ8, (1, 17, 17, 32, 8)),                # 9248-byte image
+        ((1, 40, 16, 32), 8, 32, g3, REQ8, (1, 40, 16, 32, 8)),                # 20 KB image, 16-wide rows
+        ((1, 40, 20, 64), 4, 32, g5, REQ4, (1, 40, 20, 32, 4)),                # 5x5 bands of 2-chunk taps
     ]
     for args in refused:
         assert call_conv_tiled(q, L, *args, (img, 0, 0, 0)) == 7, args

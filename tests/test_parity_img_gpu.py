@@ -224,3 +224,51 @@ def test_img_wide_many_images(qnn, orc, bits):
     """More image groups than workgroups, four 8x8 images per step."""
     L = layer(bits, 3001, 8, 8, 64, 5, 2, seed=bits, c=32)
     check(qnn, orc, L, pool=True)
+
+
+# (bits, channels, n, h, w, m, k, pad): images larger than one tile, walked
+# in bands of 8 output rows: the INT-4 batch-64 layer's shape, 5x5 filters,
+# ragged heights (a partial last band), rows of 17 to 32 outputs, no
+# padding, several and partial 32-channel groups
+BANDS = [
+    (4, 64, 2, 32, 32, 64, 3, 1),
+    (8, 32, 2, 32, 32, 32, 3, 1),
+    (8, 32, 2, 32, 32, 32, 5, 2),
+    (8, 32, 3, 27, 19, 40, 5, 2),
+    (4, 64, 2, 41, 23, 96, 3, 1),
+    (4, 64, 1, 20, 30, 32, 3, 0),
+    (8, 32, 1, 18, 17, 32, 3, 1),
+    (8, 32, 2, 30, 32, 64, 5, 0),
+]
+
+
+@pytest.mark.parametrize("pool", [False, True])
+def test_img_bands(qnn, orc, pool):
+    for i, (bits, c, n, h, w, m, k, pad) in enumerate(BANDS):
+        L = layer(bits, n, h, w, m, k, pad, seed=500 + i, c=c)
+        assert L.h * L.w * L.c * bits // 8 > 8192
+        check(qnn, orc, L, pool=pool)
+        if not pool:
+            check(qnn, orc, L, tile=IMAGE)
+            check(qnn, orc, L, epi="raw32")
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_img_band_plan_modes(qnn, orc, bits):
+    """The general plan forms and non-positive multipliers in band mode."""
+    hi = (1 << bits) - 1
+    c = 256 // bits
+    for j, kw in enumerate([dict(mult_rng=(1 << 12, 1 << 14), shift=8),
+                            dict(mult_rng=(1, 3), shift=0, clip=(1, hi - 1)),
+                            dict(mult_rng=(-(1 << 10), 1 << 10), shift=9)]):
+        L = layer(bits, 2, 26, 24, 32, 3, 1, seed=90 + j, c=c, **kw)
+        check(qnn, orc, L)
+        check(qnn, orc, L, pool=True)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_img_band_many_steps(qnn, orc, bits):
+    """More bands than resident workgroups: workgroups walk several bands of
+    different images, each prefetched during the previous one."""
+    L = layer(bits, 300, 18, 17, 32, 3, 1, seed=40 + bits, c=256 // bits)
+    check(qnn, orc, L)
