@@ -331,6 +331,17 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     int grp = blockIdx.x;
     if (grp < a.ngroups)
         issue(grp);
+    // the channel parameters of the plans (wave 0), loaded now so that their
+    // latency overlaps the image and filter loads
+    int32_t p_bias = 0, p_mult = 0, p_shift = 0;
+    if (wv == 0 && live) {
+        if (a.bias)
+            p_bias = a.bias[ch];
+        if (a.epi == EPI_REQUANT) {
+            p_mult = a.mult[ch];
+            p_shift = a.shift[ch];
+        }
+    }
 
     // ---- filters: the lane's fragment of every K step as int8 (4-/2-bit
     // weights as 16*w / 64*w) ----
@@ -350,7 +361,11 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
         constexpr int WB = G::WB, FP = G::FP, QPR = WROW / 16, UPQ = 16 / WB;
         const int nq = min(32, a.m - gy * 32) * QPR;
         const uint8_t *wg = a.w + (size_t)gy * 32 * WROW;
-        for (int q = tid; q < 32 * QPR; q += NT) {
+#pragma unroll
+        for (int i = 0; i < (32 * QPR + NT - 1) / NT; ++i) {
+            const int q = tid + i * NT;
+            if (32 * QPR % NT != 0 && q >= 32 * QPR)
+                break;
             uint4 v = make_uint4(0, 0, 0, 0);
             if (q < nq)
                 v = *(const uint4 *)(wg + (size_t)q * 16);
@@ -420,15 +435,6 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                     wsum += (int)(int8_t)d + (int)(int8_t)(d >> 8) + (int)(int8_t)(d >> 16) + (int)(int8_t)(d >> 24);
                 }
             wsum += __shfl_xor(wsum, 32, 64);  // the other lane half's share of the channel
-        }
-        int32_t p_bias = 0, p_mult = 0, p_shift = 0;
-        if (live) {
-            if (a.bias)
-                p_bias = a.bias[ch];
-            if (a.epi == EPI_REQUANT) {
-                p_mult = a.mult[ch];
-                p_shift = a.shift[ch];
-            }
         }
         int4 q0, q1;
         int64_t b = p_bias;
@@ -508,10 +514,17 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                     }
                 }
             } else {
-                // one quad is part of one pixel
-                const int ii = (int)fdiv((uint32_t)q, a.div_imgq);
-                const int qi = q - ii * imgq;
-                const int pix = (int)fdiv((uint32_t)qi, a.div_pq);
+                // one quad is part of one pixel (P / 16 quads per pixel); a
+                // band step holds one tile of a.trows rows
+                int ii, qi;
+                if constexpr (BAND) {
+                    ii = q < a.trows * a.w_ * (P / 16) ? 0 : 1;
+                    qi = q;
+                } else {
+                    ii = (int)fdiv((uint32_t)q, a.div_imgq);
+                    qi = q - ii * imgq;
+                }
+                const int pix = qi / (P / 16);
                 const int part = qi - pix * (P / 16);
                 if (ii < ni) {
                     const int iy = (int)fdiv((uint32_t)pix, a.div_w);
@@ -542,12 +555,13 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 const uint8_t *p0 = smem + ii * a.tile_bytes + 2 * tp * RT * RB + lane_slot;
                 v16i c0, c1;
                 img_steps<BITS, P, KH, KW, WOP, 0>(p0, p0 + RT * RB, A, c0, c1);
-                // an opaque zero keeps the general paths' per-register bounds
-                // checks in this body (hoisted out of the loop they would hold
-                // a lane mask per output register throughout)
-                int ez = 0;
-                __asm__ volatile("" : "+v"(ez));
-                epi(i0 + ii, orow0 + 2 * tp * RT, ez, c0, c1);
+                // an opaque copy of the lane half keeps the general paths'
+                // per-register pixel indexes and bounds checks in this body
+                // (hoisted out of the loop they would hold a register or a
+                // lane mask per output register throughout)
+                int hx = h;
+                __asm__ volatile("" : "+v"(hx));
+                epi(i0 + ii, orow0 + 2 * tp * RT, hx, c0, c1);
             }
         };
         // ---- epilogues: lane (r32, h) holds channel ch for tile pixels
@@ -558,7 +572,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
         if constexpr (POOL) {
             typedef PoolWin<WOP> PW;
             // pooled rows of the pair start at orow / 2
-            auto store_pool = [&](int img, int orow, int ez, const uint32_t *code) {
+            auto store_pool = [&](int img, int orow, int hx, const uint32_t *code) {
                 uint32_t byte[8];
 #pragma unroll
                 for (int k = 0; k < 8; ++k)
@@ -583,7 +597,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 } else {
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
-                        const int pr = (orow >> 1) + PW::prow(k), pc = PW::pcol(k) + 2 * h + ez;
+                        const int pr = (orow >> 1) + PW::prow(k), pc = PW::pcol(k) + 2 * hx;
                         if (pr < a.hp && pc < a.wp)
                             yb[((size_t)pr * a.wp + pc) * a.ypb] = (uint8_t)byte[k];
                     }
@@ -600,7 +614,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 y1 = tb[v + d + 1];
             };
             if (all3) {
-                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint32_t code[8];
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
@@ -608,10 +622,10 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                         win(k, c0, c1, x0, x1, y0, y1);
                         code[k] = img_code3(max(max(x0, x1), max(y0, y1)), e0, e1);
                     }
-                    store_pool(img, orow, ez, code);
+                    store_pool(img, orow, hx, code);
                 });
             } else if (all34) {
-                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint32_t code[8];
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
@@ -619,14 +633,14 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                         win(k, c0, c1, x0, x1, y0, y1);
                         code[k] = img_code4(max(max(x0, x1), max(y0, y1)), e0, e1);
                     }
-                    store_pool(img, orow, ez, code);
+                    store_pool(img, orow, hx, code);
                 });
             } else {
                 // rare forms (plans outside the strict form, or multipliers
                 // that are not positive): one pooled value at a time, kept
                 // rolled so their 64-bit temporaries do not crowd the
                 // registers of the fast forms
-                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint8_t *yb = a.y + (size_t)img * a.hp * a.wp * a.ypb + ch_byte;
 #pragma unroll 1
                     for (int k = 0; k < 8; ++k) {
@@ -651,21 +665,21 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                         const uint32_t byte = img_pack_lanes<BITS>(code);
                         const int pr = (orow >> 1) + (WOP == 32 ? 0 : (WOP == 16 ? k >> 2 : 2 * (k >> 2) + ((k >> 1) & 1)));
                         const int pc = (WOP == 32 ? 4 * (k >> 1) + (k & 1)
-                                                  : (WOP == 16 ? 4 * ((k & 3) >> 1) + (k & 1) : (k & 1))) + 2 * h + ez;
+                                                  : (WOP == 16 ? 4 * ((k & 3) >> 1) + (k & 1) : (k & 1))) + 2 * hx;
                         if (st_ok && pr < a.hp && pc < a.wp)
                             yb[((size_t)pr * a.wp + pc) * a.ypb] = (uint8_t)byte;
                     }
                 });
             }
         } else if (a.epi == EPI_RAW32) {
-            run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
+            run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                 if (!live)
                     return;
 #pragma unroll
                 for (int t = 0; t < 2; ++t) {
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
-                        const int p = 8 * (v >> 2) + 4 * h + (v & 3) + ez;
+                        const int p = 8 * (v >> 2) + 4 * hx + (v & 3);
                         const int oy = orow + t * RT + p / WOP, ox = p % WOP;
                         const int32_t av = t ? c1[v] : c0[v];
                         if (oy < a.ho && ox < a.wo)
@@ -675,7 +689,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 }
             });
         } else {
-            auto store_tiles = [&](int img, int orow, int ez, const uint32_t *code) {
+            auto store_tiles = [&](int img, int orow, int hx, const uint32_t *code) {
                 uint32_t byte[32];
 #pragma unroll
                 for (int v = 0; v < 32; ++v)
@@ -700,7 +714,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 } else {
 #pragma unroll
                     for (int v = 0; v < 32; ++v) {
-                        const int p = 8 * ((v & 15) >> 2) + 4 * h + (v & 3) + ez;
+                        const int p = 8 * ((v & 15) >> 2) + 4 * hx + (v & 3);
                         const int oy = orow + (v >> 4) * RT + p / WOP, ox = p % WOP;
                         if (oy < a.ho && ox < a.wo)
                             yb[((size_t)oy * a.wo + ox) * a.ypb] = (uint8_t)byte[v];
@@ -708,27 +722,27 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 }
             };
             if (all3) {
-                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint32_t code[32];
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
                         code[v] = img_code3(c0[v], e0, e1);
                         code[16 + v] = img_code3(c1[v], e0, e1);
                     }
-                    store_tiles(img, orow, ez, code);
+                    store_tiles(img, orow, hx, code);
                 });
             } else if (all34) {
-                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint32_t code[32];
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
                         code[v] = img_code4(c0[v], e0, e1);
                         code[16 + v] = img_code4(c1[v], e0, e1);
                     }
-                    store_tiles(img, orow, ez, code);
+                    store_tiles(img, orow, hx, code);
                 });
             } else {
-                run([&](int img, int orow, int ez, const v16i &c0, const v16i &c1) {
+                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint8_t *yb = a.y + (size_t)img * a.ho * a.wo * a.ypb + ch_byte;
 #pragma unroll
                     for (int t = 0; t < 2; ++t) {
@@ -736,7 +750,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                         for (int v = 0; v < 16; ++v) {
                             const uint32_t byte = img_pack_lanes<BITS>(
                                 img_code<SL>(t ? c1[v] : c0[v], e0, e1, a.clip_lo, a.clip_hi));
-                            const int p = 8 * (v >> 2) + 4 * h + (v & 3) + ez;
+                            const int p = 8 * (v >> 2) + 4 * hx + (v & 3);
                             const int oy = orow + t * RT + p / WOP, ox = p % WOP;
                             if (st_ok && oy < a.ho && ox < a.wo)
                                 yb[((size_t)oy * a.wo + ox) * a.ypb] = (uint8_t)byte;

@@ -462,7 +462,6 @@ bool plan_img(ImgArgs &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g
         p.div_w = make_fastdiv((uint32_t)x->w);
         p.div_pairs = make_fastdiv((uint32_t)p.pairs);
         p.div_imgq = make_fastdiv((uint32_t)(trows * x->w * pb / 16));
-        p.div_pq = make_fastdiv((uint32_t)(pb / 16));
         p.bands = (int32_t)bands;
         p.brows = brows;
         p.trows = trows;
@@ -506,7 +505,6 @@ bool plan_img(ImgArgs &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g
     p.div_w = make_fastdiv((uint32_t)x->w);
     p.div_pairs = make_fastdiv((uint32_t)pairs);
     p.div_imgq = make_fastdiv((uint32_t)(img_bytes / 16 > 0 ? img_bytes / 16 : 1));
-    p.div_pq = make_fastdiv((uint32_t)(pb >= 16 ? pb / 16 : 1));
     return true;
 }
 

@@ -99,7 +99,6 @@ struct ImgArgs {
     FastDiv div_w;         // input width
     FastDiv div_pairs;     // pairs
     FastDiv div_imgq;      // 16-byte quads per image
-    FastDiv div_pq;        // 16-byte quads per pixel (pixels of 16 / 32 bytes)
     // row bands (images too large for one tile): a step is one band of brows
     // output rows of one image; its tile holds trows = brows + kh - 1 input
     // rows (rows outside the image as pads) and div_imgq counts the tile's
