@@ -350,6 +350,16 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     uint8_t *sF = smem + (size_t)a.ipw * a.tile_bytes;
     int4 *sPlan = (int4 *)(sF + G::FLDS);  // [32 channels][e0, e1]
     int *sVote = (int *)(sPlan + 64);
+    // pads: every image tile holds the zero code once (staged: -128 at 8
+    // bits); each step then overwrites only its interior (bands: also their
+    // pad rows).  The barrier after the filter units also orders this fill
+    // before the first staging
+    {
+        const uint32_t f = BITS == 8 ? 0x80808080u : 0u;
+        const uint4 f4 = make_uint4(f, f, f, f);
+        for (int i = tid; i < a.ipw * a.tile_bytes / 16; i += NT)
+            ((uint4 *)smem)[i] = f4;
+    }
     v4i A[KS];
     if constexpr (G::CHUNK) {
         // the fragment of K step s (tap s / CPT, chunk s % CPT) for lane half
@@ -384,11 +394,8 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 *(uint4 *)(dst + 3 * FP) = w2_word(v.w);
             }
         }
-        __syncthreads();
-#pragma unroll
-        for (int s = 0; s < KS; ++s)
-            A[s] = *(const v4i *)(sF + (2 * s + h) * FP + r32 * 16);
-    } else {
+    }
+    if constexpr (!G::CHUNK) {
         const uint8_t *wb = a.w + (size_t)(live ? ch : 0) * WROW;
         typedef typename G::BT TP;
 #pragma unroll
@@ -419,11 +426,19 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
         }
     }
 
+    __syncthreads();
+    if constexpr (G::CHUNK) {
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+            A[s] = *(const v4i *)(sF + (2 * s + h) * G::FP + r32 * 16);
+    }
+
     // ---- the group's compression plans (requant_plan) and the wave-uniform
     // fast paths: every channel in the 32-bit strict form; in the 32- or
     // 64-bit strict form; every channel's code non-decreasing in the
     // accumulator (positive multiplier).  Computed by wave 0 (whose lanes hold
-    // the same 32 channels as every wave's) and shared through LDS ----
+    // the same 32 channels as every wave's) while the other waves stage the
+    // first step, and shared through LDS (read after the staging barrier) ----
     if (wv == 0) {
         int32_t wsum = 0;
         if (BITS == 8) {
@@ -453,19 +468,6 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             *sVote = (v3 ? 1 : 0) | (v34 ? 2 : 0) | (vm ? 4 : 0);
     }
 
-    // ---- pads: every image tile holds the zero code once (staged: -128 at
-    // 8 bits); each image then overwrites only its interior ----
-    {
-        const uint32_t f = BITS == 8 ? 0x80808080u : 0u;
-        const uint4 f4 = make_uint4(f, f, f, f);
-        for (int i = tid; i < a.ipw * a.tile_bytes / 16; i += NT)
-            ((uint4 *)smem)[i] = f4;
-    }
-    __syncthreads();
-    const int4 e0 = sPlan[2 * r32], e1 = sPlan[2 * r32 + 1];
-    const int votes = *sVote;
-    const bool all3 = (votes & 1) != 0, all34 = (votes & 2) != 0, mono = (votes & 4) != 0;
-    const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);  // raw: bias (+ 128 wsum)
 
     const bool st_ok = live && (r32 % (8 / BITS)) == 0;
     const int ch_byte = gy * 4 * BITS + ((r32 * BITS) >> 3);
@@ -541,6 +543,10 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             }
         }
         __syncthreads();
+        const int4 e0 = sPlan[2 * r32], e1 = sPlan[2 * r32 + 1];
+        const int votes = *sVote;
+        const bool all3 = (votes & 1) != 0, all34 = (votes & 2) != 0, mono = (votes & 4) != 0;
+        const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);  // raw: bias (+ 128 wsum)
         if (grp + (int)gridDim.x < a.ngroups)
             issue(grp + gridDim.x);
 
