@@ -92,10 +92,12 @@ struct ImgGeom {
     // CHUNK filters pass through LDS unpacked: fragment unit u = 2 * (K
     // step) + lane half of channel c at u * FP + 16 c (FP: one unit of all 32
     // channels, padded); FLDS bytes in all.  XLDS: the LDS beyond the image
-    // tiles (filters, then 32 plans of 32 bytes and a vote word)
+    // tiles (filters, then 32 plans of 32 bytes and a vote word, then each
+    // wave's output staging: 64 pixels of one 32-channel group, 4 * BITS
+    // bytes each)
     static constexpr int FP = 33 * 16;
     static constexpr int FLDS = CHUNK ? 2 * KS * FP : 0;
-    static constexpr int XLDS = FLDS + 64 * 16 + 16;
+    static constexpr int XLDS = FLDS + 64 * 16 + 16 + 4 * 64 * 4 * BITS;
 };
 
 // One 16-byte im2col fragment for K step S of the pixel whose tile slot is
@@ -231,6 +233,20 @@ __device__ __forceinline__ uint32_t img_pack_lanes(uint32_t code)
     return v;
 }
 
+// Copies the N = 4 * BITS code bytes of one pixel's 32-channel group from
+// LDS (16-byte aligned) to memory (aligned to N).
+template <int N>
+__device__ __forceinline__ void img_copy_group(uint8_t *dst, const uint8_t *src)
+{
+    if constexpr (N >= 16) {
+#pragma unroll
+        for (int i = 0; i < N; i += 16)
+            *(uint4 *)(dst + i) = *(const uint4 *)(src + i);
+    } else {
+        *(uint2 *)dst = *(const uint2 *)src;
+    }
+}
+
 // A compile-time int (the byte stride of an output pixel in the store fast
 // paths).
 template <int V>
@@ -350,6 +366,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     uint8_t *sF = smem + (size_t)a.ipw * a.tile_bytes;
     int4 *sPlan = (int4 *)(sF + G::FLDS);  // [32 channels][e0, e1]
     int *sVote = (int *)(sPlan + 64);
+    uint8_t *sOut = (uint8_t *)(sPlan + 65) + wv * 64 * 4 * BITS;  // this wave's output staging
     // pads: every image tile holds the zero code once (staged: -128 at 8
     // bits); each step then overwrites only its interior (bands: also their
     // pad rows).  The barrier after the filter units also orders this fill
@@ -583,17 +600,24 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
 #pragma unroll
                 for (int k = 0; k < 8; ++k)
                     byte[k] = img_pack_lanes<BITS>(code[k]);
-                if (!st_ok)
-                    return;
-                uint8_t *yb = a.y + (size_t)img * a.hp * a.wp * a.ypb + ch_byte;
                 // whole pooled rows of pixels of one or two 32-channel
-                // groups: compile-time strides (immediate store offsets)
+                // groups: the pair's 16 pooled pixels are assembled in the
+                // wave's LDS staging (no barrier: the wave reads only what it
+                // wrote) and leave as one group-wide store per pixel
                 auto fast = [&](auto yp) {
-                    constexpr int YP = decltype(yp)::value, WP = WOP / 2;
-                    uint8_t *yt = yb + ((size_t)(orow >> 1) * WP + 2 * h) * YP;
+                    constexpr int YP = decltype(yp)::value, WP = WOP / 2, YG = 4 * BITS;
+                    if (st_ok) {
 #pragma unroll
-                    for (int k = 0; k < 8; ++k)
-                        yt[(PW::prow(k) * WP + PW::pcol(k)) * YP] = (uint8_t)byte[k];
+                        for (int k = 0; k < 8; ++k)
+                            sOut[(PW::prow(k) * WP + PW::pcol(k) + 2 * h) * YG + ((r32 * BITS) >> 3)] = (uint8_t)byte[k];
+                    }
+                    __asm__ volatile("" ::: "memory");
+                    if (lane < 16) {
+                        uint8_t *yt = a.y + (size_t)img * a.hp * a.wp * a.ypb + gy * YG +
+                                      ((size_t)((orow >> 1) + lane / WP) * WP + lane % WP) * YP;
+                        img_copy_group<YG>(yt, sOut + lane * YG);
+                    }
+                    __asm__ volatile("" ::: "memory");
                 };
                 const bool rows = a.wp == WOP / 2 && (orow >> 1) + RT <= a.hp;
                 if (rows && a.ypb == 4 * BITS) {
@@ -601,6 +625,9 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 } else if (rows && a.ypb == 8 * BITS) {
                     fast(ImgConst<8 * BITS>());
                 } else {
+                    if (!st_ok)
+                        return;
+                    uint8_t *yb = a.y + (size_t)img * a.hp * a.wp * a.ypb + ch_byte;
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
                         const int pr = (orow >> 1) + PW::prow(k), pc = PW::pcol(k) + 2 * hx;
@@ -700,17 +727,23 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
 #pragma unroll
                 for (int v = 0; v < 32; ++v)
                     byte[v] = img_pack_lanes<BITS>(code[v]);
-                if (!st_ok)
-                    return;
-                uint8_t *yb = a.y + (size_t)img * a.ho * a.wo * a.ypb + ch_byte;
-                // whole rows of pixels of one or two 32-channel groups:
-                // compile-time strides (immediate store offsets)
+                // whole rows of pixels of one or two 32-channel groups: the
+                // pair's 64 pixels are assembled in the wave's LDS staging
+                // (no barrier: the wave reads only what it wrote) and each
+                // lane stores one pixel's group bytes (byte stores straight
+                // from the lanes cost 32 store instructions per wave)
                 auto fast = [&](auto yp) {
-                    constexpr int YP = decltype(yp)::value;
-                    uint8_t *yt = yb + ((size_t)orow * WOP + 4 * h) * YP;
+                    constexpr int YP = decltype(yp)::value, YG = 4 * BITS;
+                    if (st_ok) {
 #pragma unroll
-                    for (int v = 0; v < 32; ++v)
-                        yt[((v >> 4) * 32 + 8 * ((v & 15) >> 2) + (v & 3)) * YP] = (uint8_t)byte[v];
+                        for (int v = 0; v < 32; ++v)
+                            sOut[((v >> 4) * 32 + 8 * ((v & 15) >> 2) + 4 * h + (v & 3)) * YG + ((r32 * BITS) >> 3)] =
+                                (uint8_t)byte[v];
+                    }
+                    __asm__ volatile("" ::: "memory");
+                    uint8_t *yt = a.y + (size_t)img * a.ho * a.wo * a.ypb + gy * YG + ((size_t)orow * WOP + lane) * YP;
+                    img_copy_group<YG>(yt, sOut + lane * YG);
+                    __asm__ volatile("" ::: "memory");
                 };
                 const bool rows = a.wo == WOP && orow + 2 * RT <= a.ho;
                 if (rows && a.ypb == 4 * BITS) {
@@ -718,6 +751,9 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 } else if (rows && a.ypb == 8 * BITS) {
                     fast(ImgConst<8 * BITS>());
                 } else {
+                    if (!st_ok)
+                        return;
+                    uint8_t *yb = a.y + (size_t)img * a.ho * a.wo * a.ypb + ch_byte;
 #pragma unroll
                     for (int v = 0; v < 32; ++v) {
                         const int p = 8 * ((v & 15) >> 2) + 4 * hx + (v & 3);
