@@ -93,11 +93,12 @@ struct ImgGeom {
     // step) + lane half of channel c at u * FP + 16 c (FP: one unit of all 32
     // channels, padded); FLDS bytes in all.  XLDS: the LDS beyond the image
     // tiles (filters, then 32 plans of 32 bytes and a vote word, then each
-    // wave's output staging: 64 pixels of one 32-channel group, 4 * BITS
-    // bytes each)
+    // wave's output staging: 64 pixels of one 32-channel group, one code
+    // byte per channel, OPS bytes apart)
     static constexpr int FP = 33 * 16;
     static constexpr int FLDS = CHUNK ? 2 * KS * FP : 0;
-    static constexpr int XLDS = FLDS + 64 * 16 + 16 + 4 * 64 * 4 * BITS;
+    static constexpr int OPS = 48;
+    static constexpr int XLDS = FLDS + 64 * 16 + 16 + 4 * 64 * OPS;
 };
 
 // One 16-byte im2col fragment for K step S of the pixel whose tile slot is
@@ -233,17 +234,43 @@ __device__ __forceinline__ uint32_t img_pack_lanes(uint32_t code)
     return v;
 }
 
-// Copies the N = 4 * BITS code bytes of one pixel's 32-channel group from
-// LDS (16-byte aligned) to memory (aligned to N).
-template <int N>
-__device__ __forceinline__ void img_copy_group(uint8_t *dst, const uint8_t *src)
+// Packs the 32 codes of one pixel's 32-channel group (one byte each in LDS,
+// 16-byte aligned, channel order) into 4 * BITS bytes, the lower channel in
+// the lower bits, and stores them (dst aligned to 4 * BITS).
+template <int BITS>
+__device__ __forceinline__ void img_pack_store(uint8_t *dst, const uint8_t *src)
 {
-    if constexpr (N >= 16) {
+    const uint4 lo = *(const uint4 *)src, hi = *(const uint4 *)(src + 16);
+    if constexpr (BITS == 8) {
+        *(uint4 *)dst = lo;
+        *(uint4 *)(dst + 16) = hi;
+    } else if constexpr (BITS == 4) {
+        // bytes 2i and 2i + 1 -> one byte (even channel in the low nibble)
+        const uint32_t d[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        uint32_t o[4];
 #pragma unroll
-        for (int i = 0; i < N; i += 16)
-            *(uint4 *)(dst + i) = *(const uint4 *)(src + i);
+        for (int m = 0; m < 4; ++m) {
+            const uint32_t e = __builtin_amdgcn_perm(d[2 * m + 1], d[2 * m], 0x06040200u);
+            const uint32_t od = __builtin_amdgcn_perm(d[2 * m + 1], d[2 * m], 0x07050301u);
+            o[m] = e | (od << 4);
+        }
+        *(uint4 *)dst = make_uint4(o[0], o[1], o[2], o[3]);
     } else {
-        *(uint2 *)dst = *(const uint2 *)src;
+        // the four bytes of each word -> one byte, 2 bits each
+        const uint32_t d[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+        uint32_t y[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t x = d[i] | (d[i] >> 6);  // byte 0: b0 | b1 << 2, byte 2: b2 | b3 << 2
+            y[i] = x | (x >> 12);                   // byte 0: the packed byte
+        }
+        const uint32_t w0 = __builtin_amdgcn_perm(
+            __builtin_amdgcn_perm(y[3], y[2], 0x0c0c0400u), __builtin_amdgcn_perm(y[1], y[0], 0x0c0c0400u),
+            0x05040100u);
+        const uint32_t w1 = __builtin_amdgcn_perm(
+            __builtin_amdgcn_perm(y[7], y[6], 0x0c0c0400u), __builtin_amdgcn_perm(y[5], y[4], 0x0c0c0400u),
+            0x05040100u);
+        *(uint2 *)dst = make_uint2(w0, w1);
     }
 }
 
@@ -366,7 +393,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     uint8_t *sF = smem + (size_t)a.ipw * a.tile_bytes;
     int4 *sPlan = (int4 *)(sF + G::FLDS);  // [32 channels][e0, e1]
     int *sVote = (int *)(sPlan + 64);
-    uint8_t *sOut = (uint8_t *)(sPlan + 65) + wv * 64 * 4 * BITS;  // this wave's output staging
+    uint8_t *sOut = (uint8_t *)(sPlan + 65) + wv * 64 * G::OPS;  // this wave's output staging
     // pads: every image tile holds the zero code once (staged: -128 at 8
     // bits); each step then overwrites only its interior (bands: also their
     // pad rows).  The barrier after the filter units also orders this fill
@@ -601,9 +628,12 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 for (int k = 0; k < 8; ++k)
                     byte[k] = img_pack_lanes<BITS>(code[k]);
                 // whole pooled rows of pixels of one or two 32-channel
-                // groups: the pair's 16 pooled pixels are assembled in the
-                // wave's LDS staging (no barrier: the wave reads only what it
-                // wrote) and leave as one group-wide store per pixel
+                // groups: the pair's 16 pooled pixels are assembled (packed
+                // across lanes) in the wave's LDS staging (no barrier: the
+                // wave reads only what it wrote) and leave as one group-wide
+                // store per pixel.  (Packing them on the read-back instead,
+                // as the unpooled path does, costs the one-word-pixel
+                // instances 20-30 registers and a wave per SIMD)
                 auto fast = [&](auto yp) {
                     constexpr int YP = decltype(yp)::value, WP = WOP / 2, YG = 4 * BITS;
                     if (st_ok) {
@@ -615,7 +645,13 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                     if (lane < 16) {
                         uint8_t *yt = a.y + (size_t)img * a.hp * a.wp * a.ypb + gy * YG +
                                       ((size_t)((orow >> 1) + lane / WP) * WP + lane % WP) * YP;
-                        img_copy_group<YG>(yt, sOut + lane * YG);
+                        if constexpr (YG >= 16) {
+#pragma unroll
+                            for (int i = 0; i < YG; i += 16)
+                                *(uint4 *)(yt + i) = *(const uint4 *)(sOut + lane * YG + i);
+                        } else {
+                            *(uint2 *)yt = *(const uint2 *)(sOut + lane * YG);
+                        }
                     }
                     __asm__ volatile("" ::: "memory");
                 };
@@ -723,26 +759,21 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             });
         } else {
             auto store_tiles = [&](int img, int orow, int hx, const uint32_t *code) {
-                uint32_t byte[32];
-#pragma unroll
-                for (int v = 0; v < 32; ++v)
-                    byte[v] = img_pack_lanes<BITS>(code[v]);
-                // whole rows of pixels of one or two 32-channel groups: the
-                // pair's 64 pixels are assembled in the wave's LDS staging
-                // (no barrier: the wave reads only what it wrote) and each
-                // lane stores one pixel's group bytes (byte stores straight
-                // from the lanes cost 32 store instructions per wave)
+                // whole rows of pixels of one or two 32-channel groups: every
+                // lane writes its channel's code bytes into the wave's LDS
+                // staging (no barrier: the wave reads only what it wrote);
+                // each lane then packs one of the pair's 64 pixels and stores
+                // it with one group-wide store (packing across lanes and byte
+                // stores straight from them cost 2-4 vector instructions per
+                // code and 32 store instructions per wave)
                 auto fast = [&](auto yp) {
                     constexpr int YP = decltype(yp)::value, YG = 4 * BITS;
-                    if (st_ok) {
 #pragma unroll
-                        for (int v = 0; v < 32; ++v)
-                            sOut[((v >> 4) * 32 + 8 * ((v & 15) >> 2) + 4 * h + (v & 3)) * YG + ((r32 * BITS) >> 3)] =
-                                (uint8_t)byte[v];
-                    }
+                    for (int v = 0; v < 32; ++v)
+                        sOut[((v >> 4) * 32 + 8 * ((v & 15) >> 2) + 4 * h + (v & 3)) * G::OPS + r32] = (uint8_t)code[v];
                     __asm__ volatile("" ::: "memory");
                     uint8_t *yt = a.y + (size_t)img * a.ho * a.wo * a.ypb + gy * YG + ((size_t)orow * WOP + lane) * YP;
-                    img_copy_group<YG>(yt, sOut + lane * YG);
+                    img_pack_store<BITS>(yt, sOut + lane * G::OPS);
                     __asm__ volatile("" ::: "memory");
                 };
                 const bool rows = a.wo == WOP && orow + 2 * RT <= a.ho;
@@ -751,6 +782,10 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 } else if (rows && a.ypb == 8 * BITS) {
                     fast(ImgConst<8 * BITS>());
                 } else {
+                    uint32_t byte[32];
+#pragma unroll
+                    for (int v = 0; v < 32; ++v)
+                        byte[v] = img_pack_lanes<BITS>(code[v]);
                     if (!st_ok)
                         return;
                     uint8_t *yb = a.y + (size_t)img * a.ho * a.wo * a.ypb + ch_byte;
