@@ -1,7 +1,8 @@
 // Implicit-GEMM quantized convolution for small images: a workgroup keeps
 // whole padded images in LDS and its filters in registers.  Same computation
 // as the other convolution kernels (Sec. III-A Eq. (2), Sec. III-B Eq. (6),
-// scale-and-clamp compression, Sec. IV-A fused max-pooling), laid out for
+// scale-and-clamp compression or the staircase of Eq. (4), Sec. IV-A fused
+// max-pooling), laid out for
 // layers whose per-tile bookkeeping would dominate the general kernels: a
 // network's first layer (K = kh*kw*3 for 3 image channels) and the later
 // layers of a small network (16x16 and 8x8 images of 32 channels).
@@ -92,13 +93,13 @@ struct ImgGeom {
     // CHUNK filters pass through LDS unpacked: fragment unit u = 2 * (K
     // step) + lane half of channel c at u * FP + 16 c (FP: one unit of all 32
     // channels, padded); FLDS bytes in all.  XLDS: the LDS beyond the image
-    // tiles (filters, then 32 plans of 32 bytes and a vote word, then each
-    // wave's output staging: 64 pixels of one 32-channel group, one code
-    // byte per channel, OPS bytes apart)
+    // tiles (filters, then 32 channel plans of 64 bytes and a vote word,
+    // then each wave's output staging: 64 pixels of one 32-channel group, one
+    // code byte per channel, OPS bytes apart)
     static constexpr int FP = 33 * 16;
     static constexpr int FLDS = CHUNK ? 2 * KS * FP : 0;
     static constexpr int OPS = 48;
-    static constexpr int XLDS = FLDS + 64 * 16 + 16 + 4 * 64 * OPS;
+    static constexpr int XLDS = FLDS + 32 * 64 + 16 + 4 * 64 * OPS;
 };
 
 // One 16-byte im2col fragment for K step S of the pixel whose tile slot is
@@ -307,9 +308,10 @@ struct PoolWin {
     }
 };
 
-template <int BITS, int P, int KH, int KW, int WOP, bool POOL, bool BAND>
+template <int BITS, int P, int KH, int KW, int WOP, bool POOL, bool BAND, bool STAIR>
 __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
 {
+    static_assert(!STAIR || BITS != 8, "the staircase epilogue is built at 4 and 2 bits");
     typedef ImgGeom<BITS, P, KH, KW, WOP> G;
     static_assert(!BAND || P >= 16, "row bands are built for pixels of whole 16-byte quads");
     constexpr int NW = 4, NT = 256;
@@ -391,9 +393,16 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     // LDS behind the image tiles: the unpacked filter units (CHUNK), then the
     // group's compression plans and fast-path votes
     uint8_t *sF = smem + (size_t)a.ipw * a.tile_bytes;
-    int4 *sPlan = (int4 *)(sF + G::FLDS);  // [32 channels][e0, e1]
-    int *sVote = (int *)(sPlan + 64);
-    uint8_t *sOut = (uint8_t *)(sPlan + 65) + wv * 64 * G::OPS;  // this wave's output staging
+    // the requantization plans (e0 of the 32 channels, then their e1: lanes
+    // read consecutive 16-byte entries), or [32 channels][16] staircase
+    // thresholds on the kernel's accumulator scale
+    int4 *sPlan = (int4 *)(sF + G::FLDS);
+    int *sVote = (int *)(sPlan + 128);
+    uint8_t *sOut = (uint8_t *)(sPlan + 129) + wv * 64 * G::OPS;  // this wave's output staging
+    constexpr int NTH = (1 << BITS) - 1;  // staircase thresholds per channel (4 and 2 bits)
+    // STAIR instances compute only the staircase (Eq. (4)); the others every
+    // other epilogue (a separate instance keeps each one's code small)
+    constexpr bool stair = STAIR;
     // pads: every image tile holds the zero code once (staged: -128 at 8
     // bits); each step then overwrites only its interior (bands: also their
     // pad rows).  The barrier after the filter units also orders this fill
@@ -495,21 +504,35 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 }
             wsum += __shfl_xor(wsum, 32, 64);  // the other lane half's share of the channel
         }
-        int4 q0, q1;
-        int64_t b = p_bias;
-        if (BITS == 8)
-            b += 128 * (int64_t)wsum;
-        const int sh = p_shift < 0 ? 0 : (p_shift > 62 ? 62 : p_shift);
-        requant_plan(b, p_mult, sh, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, SL, q0, q1);
-        const bool v3 = __all(!live || q1.z == 3);
-        const bool v34 = __all(!live || q1.z == 3 || q1.z == 4);
-        const bool vm = __all(!live || q1.z != 0 || q0.z > 0);
-        if (h == 0) {
-            sPlan[2 * r32] = q0;
-            sPlan[2 * r32 + 1] = q1;
+        if constexpr (stair) {
+            // staircase (Eq. (4)): the thresholds moved onto the scaled
+            // accumulator, S (tau - bias) clamped to int32 (stair_thresholds)
+            __align__(16) int32_t T16[16];
+            stair_thresholds(live ? a.thresh + (size_t)ch * NTH : nullptr, NTH, p_bias, SL, T16);
+            if (h == 0) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    sPlan[4 * r32 + k] = make_int4(T16[4 * k], T16[4 * k + 1], T16[4 * k + 2], T16[4 * k + 3]);
+            }
+            if (lane == 0)
+                *sVote = 0;
+        } else {
+            int4 q0, q1;
+            int64_t b = p_bias;
+            if (BITS == 8)
+                b += 128 * (int64_t)wsum;
+            const int sh = p_shift < 0 ? 0 : (p_shift > 62 ? 62 : p_shift);
+            requant_plan(b, p_mult, sh, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, SL, q0, q1);
+            const bool v3 = __all(!live || q1.z == 3);
+            const bool v34 = __all(!live || q1.z == 3 || q1.z == 4);
+            const bool vm = __all(!live || q1.z != 0 || q0.z > 0);
+            if (h == 0) {
+                sPlan[r32] = q0;
+                sPlan[32 + r32] = q1;
+            }
+            if (lane == 0)
+                *sVote = (v3 ? 1 : 0) | (v34 ? 2 : 0) | (vm ? 4 : 0);
         }
-        if (lane == 0)
-            *sVote = (v3 ? 1 : 0) | (v34 ? 2 : 0) | (vm ? 4 : 0);
     }
 
 
@@ -587,7 +610,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             }
         }
         __syncthreads();
-        const int4 e0 = sPlan[2 * r32], e1 = sPlan[2 * r32 + 1];
+        const int4 e0 = sPlan[r32], e1 = sPlan[32 + r32];
         const int votes = *sVote;
         const bool all3 = (votes & 1) != 0, all34 = (votes & 2) != 0, mono = (votes & 4) != 0;
         const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);  // raw: bias (+ 128 wsum)
@@ -613,6 +636,14 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 __asm__ volatile("" : "+v"(hx));
                 epi(i0 + ii, orow0 + 2 * tp * RT, hx, c0, c1);
             }
+        };
+        // the lane's staircase thresholds (read per step: registers only in
+        // the staircase epilogue)
+        auto stair_T = [&](int32_t *T) {
+            const int32_t *src = (const int32_t *)(sPlan + 4 * r32);
+#pragma unroll
+            for (int k = 0; k < NTH; ++k)
+                T[k] = src[k];
         };
         // ---- epilogues: lane (r32, h) holds channel ch for tile pixels
         // p = 8*(v/4) + 4h + v%4 (register v): image row T*RT + p/WOP,
@@ -682,7 +713,22 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 y0 = tb[v + d];
                 y1 = tb[v + d + 1];
             };
-            if (all3) {
+            if constexpr (stair) {
+                // the level is non-decreasing in the accumulator for any
+                // thresholds: the window's maximum is counted
+                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
+                    int32_t T[NTH];
+                    stair_T(T);
+                    uint32_t code[8];
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        int32_t x0, x1, y0, y1;
+                        win(k, c0, c1, x0, x1, y0, y1);
+                        code[k] = stair_level<NTH>(max(max(x0, x1), max(y0, y1)), T);
+                    }
+                    store_pool(img, orow, hx, code);
+                });
+            } else if (all3) {
                 run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint32_t code[8];
 #pragma unroll
@@ -740,7 +786,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                     }
                 });
             }
-        } else if (a.epi == EPI_RAW32) {
+        } else if (!stair && a.epi == EPI_RAW32) {
             run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                 if (!live)
                     return;
@@ -798,7 +844,19 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                     }
                 }
             };
-            if (all3) {
+            if constexpr (stair) {
+                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
+                    int32_t T[NTH];
+                    stair_T(T);
+                    uint32_t code[32];
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        code[v] = stair_level<NTH>(c0[v], T);
+                        code[16 + v] = stair_level<NTH>(c1[v], T);
+                    }
+                    store_tiles(img, orow, hx, code);
+                });
+            } else if (all3) {
                 run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint32_t code[32];
 #pragma unroll
@@ -863,9 +921,16 @@ template <int BITS, int P, int K, int WOP, bool BAND = false>
 hipError_t launch_img(const ImgArgs &a, int cus, hipStream_t s)
 {
     constexpr int FLDS = ImgGeom<BITS, P, K, K, WOP>::XLDS;
+    if constexpr (BITS != 8) {
+        if (a.epi == EPI_STAIR) {
+            if (a.pool)
+                return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, true, BAND, true>, a, FLDS, cus, s);
+            return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, false, BAND, true>, a, FLDS, cus, s);
+        }
+    }
     if (a.pool)
-        return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, true, BAND>, a, FLDS, cus, s);
-    return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, false, BAND>, a, FLDS, cus, s);
+        return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, true, BAND, false>, a, FLDS, cus, s);
+    return launch_img_grid(conv_img_kernel<BITS, P, K, K, WOP, false, BAND, false>, a, FLDS, cus, s);
 }
 
 }  // namespace qnn

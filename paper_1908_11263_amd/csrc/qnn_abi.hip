@@ -387,7 +387,8 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
 }
 
 // Whole-image kernel (conv_img_kernel): stride 1, 3x3 or 5x5 filters, output
-// rows of at most 32 pixels, scale-and-clamp (pooled or not) or raw outputs,
+// rows of at most 32 pixels, scale-and-clamp or (4 and 2 bits) staircase
+// outputs (pooled or not) or raw outputs,
 // channel groups that fill whole output words, and pixels of
 //   * 4 packed bytes (8, 4 or 2 bits: a network's first layer), or
 //   * 16 / 32 packed bytes whose unpacked pixel is a whole number of 32-byte
@@ -408,7 +409,8 @@ bool plan_img(ImgArgs &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g
         return false;
     if (!(g->kh == g->kw && (g->kh == 3 || g->kh == 5)))
         return false;
-    if (!(e->kind == QNN_EPI_REQUANT || (e->kind == QNN_EPI_RAW32 && !pool)))
+    if (!(e->kind == QNN_EPI_REQUANT || (e->kind == QNN_EPI_RAW32 && !pool) ||
+          (e->kind == QNN_EPI_STAIR && bits != 8)))
         return false;
     if (((int64_t)m * bits) % 32 != 0 || wo > 32)
         return false;
@@ -446,6 +448,7 @@ bool plan_img(ImgArgs &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g
         p.bias = e->bias;
         p.mult = e->mult;
         p.shift = e->shift;
+        p.thresh = e->thresh;
         p.n = x->n; p.h = x->h; p.w_ = x->w; p.m = m;
         p.ph = g->pad_h; p.pw = g->pad_w; p.ho = ho; p.wo = wo;
         p.epi = e->kind;
@@ -489,6 +492,7 @@ bool plan_img(ImgArgs &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g
     p.bias = e->bias;
     p.mult = e->mult;
     p.shift = e->shift;
+    p.thresh = e->thresh;
     p.n = x->n; p.h = x->h; p.w_ = x->w; p.m = m;
     p.ph = g->pad_h; p.pw = g->pad_w; p.ho = ho; p.wo = wo;
     p.epi = e->kind;

@@ -105,6 +105,7 @@ struct ImgArgs {
     // quads.  bands = 0 in whole-image mode.
     int32_t bands, brows, trows;
     FastDiv div_bands;
+    const int32_t *thresh; // staircase thresholds [M][2^bits - 1] (EPI_STAIR)
 };
 
 // Arguments of the INT-1 XNOR/popcount convolution.

@@ -44,6 +44,8 @@ def run(qnn, L, pool=False, tile=None, epi=None):
     epi = epi or L.epi
     args = (dev(L.x), (L.n, L.h, L.w, L.c), L.bits, dev(L.wt), L.m, L.kh, L.kw, L.stride, L.pad, epi)
     kw = dict(bias=dev(L.bias), mult=dev(L.mult), shift=dev(L.shift), clip=L.clip)
+    if L.thresh is not None:
+        kw["thresh"] = dev(L.thresh)
     if pool:
         assert tile is None
         y = qnn.conv2d_maxpool(*args, **kw)
@@ -272,3 +274,53 @@ def test_img_band_many_steps(qnn, orc, bits):
     different images, each prefetched during the previous one."""
     L = layer(bits, 300, 18, 17, 32, 3, 1, seed=40 + bits, c=256 // bits)
     check(qnn, orc, L)
+
+
+def stair_img_layer(bits, c, n, h, w, m, k, pad, seed, sorted_=True):
+    """Staircase layer (Sec. III-A, Eq. (4)): 2^bits - 1 thresholds per
+    channel over a quarter of the accumulator range, sorted or not."""
+    hi = (1 << bits) - 1
+    whi = (1 << (bits - 1)) - 1
+    span = max(1, k * k * c * hi * whi // 4)
+    return synth.conv_layer("img_stair_int%d_c%d" % (bits, c), bits, n, h, w, c, m, k, pad, seed, (0, hi),
+                            (-(1 << (bits - 1)), whi), bias_rng=(-hi * 64, hi * 64),
+                            thresh_rng=(-span, span), epi="stair", stair_sorted=sorted_)
+
+
+# (bits, channels, n, h, w, m, k, pad): one-word pixels (a first layer's
+# shape; ragged, two channel groups), 16- and 32-byte pixels (5x5, a partial
+# group), and row bands (the INT-4 batch-64 layer's shape, a ragged band)
+STAIR = [
+    (4, 8, 3, 32, 32, 32, 5, 2),
+    (2, 16, 2, 17, 13, 64, 3, 1),
+    (4, 32, 3, 16, 16, 32, 5, 2),
+    (4, 64, 2, 12, 9, 24, 3, 1),
+    (2, 64, 3, 9, 16, 32, 3, 1),
+    (4, 64, 2, 32, 32, 64, 3, 1),
+    (4, 64, 1, 27, 19, 40, 3, 1),
+]
+
+
+@pytest.mark.parametrize("pool", [False, True])
+def test_img_stair(qnn, orc, pool):
+    """The staircase epilogue on the image kernel, plain and fused with
+    pooling (taken on the accumulators: the level is non-decreasing in the
+    accumulator for any thresholds), forced and by the library's choice."""
+    for i, (bits, c, n, h, w, m, k, pad) in enumerate(STAIR):
+        L = stair_img_layer(bits, c, n, h, w, m, k, pad, seed=600 + i)
+        if pool and (L.ho < 2 or L.wo < 2):
+            continue
+        check(qnn, orc, L, pool=pool)
+        if not pool:
+            check(qnn, orc, L, tile=IMAGE)
+
+
+def test_img_stair_unsorted(qnn, orc):
+    """Unsorted thresholds: the output counts the thresholds at or below the
+    biased accumulator."""
+    for i, (bits, c, n, h, w, m, k, pad) in enumerate(STAIR[::2]):
+        L = stair_img_layer(bits, c, n, h, w, m, k, pad, seed=700 + i, sorted_=False)
+        check(qnn, orc, L, tile=IMAGE)
+        if L.ho >= 2 and L.wo >= 2:
+            check(qnn, orc, L, pool=True)
+
