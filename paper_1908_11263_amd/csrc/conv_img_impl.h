@@ -275,6 +275,33 @@ __device__ __forceinline__ void img_pack_store(uint8_t *dst, const uint8_t *src)
     }
 }
 
+// Staircase level of a (scaled) accumulator for non-decreasing thresholds:
+// the balanced comparison tree of Sec. III-A (Eq. (4)), ceil(log2(NT + 1))
+// comparisons, each choosing the next threshold with selects (no indexing).
+// Equals the number of thresholds at or below acc (stair_level) whenever the
+// thresholds are sorted.
+template <int NT>
+__device__ __forceinline__ uint32_t stair_tree(int32_t acc, const int32_t *T)
+{
+    if constexpr (NT == 15) {
+        const bool c3 = acc >= T[7];
+        const bool c2 = acc >= (c3 ? T[11] : T[3]);
+        const int32_t u = c3 ? T[9] : T[1], v = c3 ? T[13] : T[5];
+        const bool c1 = acc >= (c2 ? v : u);
+        const int32_t a0 = c3 ? T[8] : T[0], a1 = c3 ? T[10] : T[2], a2 = c3 ? T[12] : T[4],
+                      a3 = c3 ? T[14] : T[6];
+        const int32_t b0 = c2 ? a2 : a0, b1 = c2 ? a3 : a1;
+        const bool c0 = acc >= (c1 ? b1 : b0);
+        return (c3 ? 8u : 0u) | (c2 ? 4u : 0u) | (c1 ? 2u : 0u) | (c0 ? 1u : 0u);
+    } else if constexpr (NT == 3) {
+        const bool c1 = acc >= T[1];
+        const bool c0 = acc >= (c1 ? T[2] : T[0]);
+        return (c1 ? 2u : 0u) | (c0 ? 1u : 0u);
+    } else {
+        return stair_level<NT>(acc, T);
+    }
+}
+
 // A compile-time int (the byte stride of an output pixel in the store fast
 // paths).
 template <int V>
@@ -514,8 +541,15 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 for (int k = 0; k < 4; ++k)
                     sPlan[4 * r32 + k] = make_int4(T16[4 * k], T16[4 * k + 1], T16[4 * k + 2], T16[4 * k + 3]);
             }
+            // every channel's thresholds non-decreasing (the scaling and the
+            // clamp keep their order): the comparison tree applies
+            bool sorted = true;
+#pragma unroll
+            for (int k = 0; k + 1 < NTH; ++k)
+                sorted = sorted && T16[k] <= T16[k + 1];
+            const bool vs = __all(sorted);
             if (lane == 0)
-                *sVote = 0;
+                *sVote = vs ? 8 : 0;
         } else {
             int4 q0, q1;
             int64_t b = p_bias;
@@ -716,18 +750,25 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             if constexpr (stair) {
                 // the level is non-decreasing in the accumulator for any
                 // thresholds: the window's maximum is counted
-                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
-                    int32_t T[NTH];
-                    stair_T(T);
-                    uint32_t code[8];
+                auto stair_pool = [&](auto tree) {
+                    run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
+                        int32_t T[NTH];
+                        stair_T(T);
+                        uint32_t code[8];
 #pragma unroll
-                    for (int k = 0; k < 8; ++k) {
-                        int32_t x0, x1, y0, y1;
-                        win(k, c0, c1, x0, x1, y0, y1);
-                        code[k] = stair_level<NTH>(max(max(x0, x1), max(y0, y1)), T);
-                    }
-                    store_pool(img, orow, hx, code);
-                });
+                        for (int k = 0; k < 8; ++k) {
+                            int32_t x0, x1, y0, y1;
+                            win(k, c0, c1, x0, x1, y0, y1);
+                            const int32_t mx = max(max(x0, x1), max(y0, y1));
+                            code[k] = decltype(tree)::value ? stair_tree<NTH>(mx, T) : stair_level<NTH>(mx, T);
+                        }
+                        store_pool(img, orow, hx, code);
+                    });
+                };
+                if (votes & 8)
+                    stair_pool(ImgConst<1>());
+                else
+                    stair_pool(ImgConst<0>());
             } else if (all3) {
                 run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint32_t code[8];
@@ -845,17 +886,30 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 }
             };
             if constexpr (stair) {
-                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
-                    int32_t T[NTH];
-                    stair_T(T);
-                    uint32_t code[32];
+                // sorted thresholds (every channel): the comparison tree;
+                // otherwise the count
+                auto stair_tiles = [&](auto tree) {
+                    run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
+                        int32_t T[NTH];
+                        stair_T(T);
+                        uint32_t code[32];
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        code[v] = stair_level<NTH>(c0[v], T);
-                        code[16 + v] = stair_level<NTH>(c1[v], T);
-                    }
-                    store_tiles(img, orow, hx, code);
-                });
+                        for (int v = 0; v < 16; ++v) {
+                            if (decltype(tree)::value) {
+                                code[v] = stair_tree<NTH>(c0[v], T);
+                                code[16 + v] = stair_tree<NTH>(c1[v], T);
+                            } else {
+                                code[v] = stair_level<NTH>(c0[v], T);
+                                code[16 + v] = stair_level<NTH>(c1[v], T);
+                            }
+                        }
+                        store_tiles(img, orow, hx, code);
+                    });
+                };
+                if (votes & 8)
+                    stair_tiles(ImgConst<1>());
+                else
+                    stair_tiles(ImgConst<0>());
             } else if (all3) {
                 run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint32_t code[32];
