@@ -1,11 +1,12 @@
 // Implicit-GEMM quantized convolution for small images: a workgroup keeps
-// whole padded images in LDS and its filters in registers.  Same computation
-// as the other convolution kernels (Sec. III-A Eq. (2), Sec. III-B Eq. (6),
-// scale-and-clamp compression or the staircase of Eq. (4), Sec. IV-A fused
-// max-pooling), laid out for
-// layers whose per-tile bookkeeping would dominate the general kernels: a
-// network's first layer (K = kh*kw*3 for 3 image channels) and the later
-// layers of a small network (16x16 and 8x8 images of 32 channels).
+// whole padded images (or row bands of larger ones) in LDS and its filters in
+// registers.  Same computation as the other convolution kernels (Sec. III-A
+// Eq. (2), Sec. III-B Eq. (6), scale-and-clamp compression or the staircase
+// of Eq. (4), Sec. IV-A fused max-pooling), laid out for layers whose
+// per-tile bookkeeping would dominate the general kernels: a network's first
+// layer (K = kh*kw*3 for 3 image channels), the later layers of a small
+// network (16x16 and 8x8 images of 32 channels) and layers with about one
+// general tile per compute unit (32x32x64 images at batch 64, in row bands).
 //   * A workgroup owns one 32-channel group (grid.y) and walks groups of
 //     whole images (several small images per step so that every wave has
 //     work): each padded image is staged once in LDS, unpacked to int8 (8-bit
@@ -17,7 +18,9 @@
 //   * The filters of the group live in registers for the whole kernel (one
 //     16-byte fragment per lane and K step); wide-pixel filters arrive
 //     through LDS once (coalesced loads of the group's rows, expanded to
-//     int8 there), and the group's compression plans are computed once.
+//     int8 there), and the group's compression plans (or staircase
+//     thresholds) are computed once, by wave 0, while the first step is
+//     staged.
 //   * A wave computes two MFMA row tiles of 32 output pixels at a time with
 //     v_mfma_i32_32x32x32_i8 (rows = pixels, columns = channels).  A row tile
 //     is 1, 2 or 4 output rows of an image WOP = 32, 16 or 8 pixels wide
@@ -34,13 +37,16 @@
 //     is two aligned 8-byte reads.
 //   * The 2x2 max-pooling is taken on the accumulators (the compression is
 //     non-decreasing in the accumulator whenever the multiplier is positive,
-//     so the maximum commutes with it) and only the pooled values are
-//     compressed; with a non-positive multiplier each code is compressed
-//     first and the codes are pooled.  The four outputs of a window always
-//     sit in one lane.
-//   * Codes leave as bytes straight from the lanes (4-/2-bit codes of
-//     neighbouring channels packed across lanes with DPP moves), with no
-//     staging through LDS.
+//     and the staircase level always is, so the maximum commutes with it)
+//     and only the pooled values are compressed; with a non-positive
+//     multiplier each code is compressed first and the codes are pooled.
+//     The four outputs of a window always sit in one lane.
+//   * Outputs in whole rows of pixels of one or two 32-channel groups are
+//     assembled per wave in LDS and leave as one group-wide store per pixel
+//     (unpooled: unpacked code bytes, packed on the read-back with byte
+//     permutes; pooled: codes of neighbouring channels packed across lanes
+//     with DPP moves first); other shapes store bytes straight from the
+//     lanes.
 #pragma once
 
 #include "conv_m32_impl.h"
