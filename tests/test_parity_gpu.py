@@ -218,10 +218,14 @@ def test_linear(qnn, orc, bits):
         x = synth.pack_codes(synth.to_code(xv, bits, False), bits)
         wt = synth.pack_codes(synth.to_code(wv, bits, True), bits)
         bias = rng.integers(-1000, 1000, size=m).astype(np.int32)
-        log("case linear bits=%d n=%d k=%d m=%d" % (bits, n, h * w * c, m))
+        # every other case without a bias (NULL: zero)
+        if m % 2 == 0:
+            bias = None
+        log("case linear bits=%d n=%d k=%d m=%d bias=%s" % (bits, n, h * w * c, m, bias is not None))
         y = qnn.linear(dev(x), (n, h, w, c), bits, dev(wt), m, "raw32", bias=dev(bias))
         torch.cuda.synchronize()
-        _, want = orc.linear(x.reshape(n, -1), n, h * w * c, bits, wt, m, epi=2, bias=bias)
+        _, want = orc.linear(x.reshape(n, -1), n, h * w * c, bits, wt, m, epi=2,
+                             bias=bias if bias is not None else np.zeros(m, np.int32))
         assert np.array_equal(y.cpu().numpy().reshape(n, m), want)
 
 
