@@ -231,7 +231,8 @@ def test_img_wide_many_images(qnn, orc, bits):
 # (bits, channels, n, h, w, m, k, pad): images larger than one tile, walked
 # in bands of 8 output rows: the INT-4 batch-64 layer's shape, 5x5 filters,
 # ragged heights (a partial last band), rows of 17 to 32 outputs, no
-# padding, several and partial 32-channel groups
+# padding and padding wider than the filter's half (halo rows above and
+# below the image in two bands), several and partial 32-channel groups
 BANDS = [
     (4, 64, 2, 32, 32, 64, 3, 1),
     (8, 32, 2, 32, 32, 32, 3, 1),
@@ -241,6 +242,7 @@ BANDS = [
     (4, 64, 1, 20, 30, 32, 3, 0),
     (8, 32, 1, 18, 17, 32, 3, 1),
     (8, 32, 2, 30, 32, 64, 5, 0),
+    (8, 32, 1, 20, 26, 32, 3, 3),
 ]
 
 
