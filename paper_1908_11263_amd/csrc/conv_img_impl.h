@@ -446,7 +446,68 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
         for (int i = tid; i < a.ipw * a.tile_bytes / 16; i += NT)
             ((uint4 *)smem)[i] = f4;
     }
+    // ---- the group's compression plans (requant_plan) and the wave-uniform
+    // fast paths: every channel in the 32-bit strict form; in the 32- or
+    // 64-bit strict form; every channel's code non-decreasing in the
+    // accumulator (positive multiplier).  Computed by wave 0 (whose lanes hold
+    // the same 32 channels as every wave's) and shared through LDS (read
+    // after the first staging barrier).  Sub-byte plans need no filter sums:
+    // wave 0 computes them before the filter staging, which the other waves
+    // do; 8-bit plans follow the filter fragments, while the other waves
+    // stage the first step ----
     v4i A[KS];
+    auto compute_plans = [&]() {
+        int32_t wsum = 0;
+        if (BITS == 8) {
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t d = (uint32_t)A[s][i];
+                    wsum += (int)(int8_t)d + (int)(int8_t)(d >> 8) + (int)(int8_t)(d >> 16) + (int)(int8_t)(d >> 24);
+                }
+            wsum += __shfl_xor(wsum, 32, 64);  // the other lane half's share of the channel
+        }
+        if constexpr (stair) {
+            // staircase (Eq. (4)): the thresholds moved onto the scaled
+            // accumulator, S (tau - bias) clamped to int32 (stair_thresholds)
+            __align__(16) int32_t T16[16];
+            stair_thresholds(live ? a.thresh + (size_t)ch * NTH : nullptr, NTH, p_bias, SL, T16);
+            if (h == 0) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    sPlan[4 * r32 + k] = make_int4(T16[4 * k], T16[4 * k + 1], T16[4 * k + 2], T16[4 * k + 3]);
+            }
+            // every channel's thresholds non-decreasing (the scaling and the
+            // clamp keep their order): the comparison tree applies
+            bool sorted = true;
+#pragma unroll
+            for (int k = 0; k + 1 < NTH; ++k)
+                sorted = sorted && T16[k] <= T16[k + 1];
+            const bool vs = __all(sorted);
+            if (lane == 0)
+                *sVote = vs ? 8 : 0;
+        } else {
+            int4 q0, q1;
+            int64_t b = p_bias;
+            if (BITS == 8)
+                b += 128 * (int64_t)wsum;
+            const int sh = p_shift < 0 ? 0 : (p_shift > 62 ? 62 : p_shift);
+            requant_plan(b, p_mult, sh, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, SL, q0, q1);
+            const bool v3 = __all(!live || q1.z == 3);
+            const bool v34 = __all(!live || q1.z == 3 || q1.z == 4);
+            const bool vm = __all(!live || q1.z != 0 || q0.z > 0);
+            if (h == 0) {
+                sPlan[r32] = q0;
+                sPlan[32 + r32] = q1;
+            }
+            if (lane == 0)
+                *sVote = (v3 ? 1 : 0) | (v34 ? 2 : 0) | (vm ? 4 : 0);
+        }
+    };
+    constexpr bool early_plans = BITS != 8;
+    if (early_plans && wv == 0)
+        compute_plans();
     if constexpr (G::CHUNK) {
         // the fragment of K step s (tap s / CPT, chunk s % CPT) for lane half
         // h is packed bytes [(2 s + h) * WB, + WB) of the channel's row: unit
@@ -457,10 +518,13 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
         constexpr int WB = G::WB, FP = G::FP, QPR = WROW / 16, UPQ = 16 / WB;
         const int nq = min(32, a.m - gy * 32) * QPR;
         const uint8_t *wg = a.w + (size_t)gy * 32 * WROW;
+        // staged by the threads of waves 1-3 when wave 0 computes the plans
+        constexpr int FT = early_plans ? NT - 64 : NT;
+        const int ft = early_plans ? tid - 64 : tid;
 #pragma unroll
-        for (int i = 0; i < (32 * QPR + NT - 1) / NT; ++i) {
-            const int q = tid + i * NT;
-            if (32 * QPR % NT != 0 && q >= 32 * QPR)
+        for (int i = 0; i < (32 * QPR + FT - 1) / FT; ++i) {
+            const int q = ft + i * FT;
+            if (ft < 0 || (32 * QPR % FT != 0 && q >= 32 * QPR))
                 break;
             uint4 v = make_uint4(0, 0, 0, 0);
             if (q < nq)
@@ -519,62 +583,8 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             A[s] = *(const v4i *)(sF + (2 * s + h) * G::FP + r32 * 16);
     }
 
-    // ---- the group's compression plans (requant_plan) and the wave-uniform
-    // fast paths: every channel in the 32-bit strict form; in the 32- or
-    // 64-bit strict form; every channel's code non-decreasing in the
-    // accumulator (positive multiplier).  Computed by wave 0 (whose lanes hold
-    // the same 32 channels as every wave's) while the other waves stage the
-    // first step, and shared through LDS (read after the staging barrier) ----
-    if (wv == 0) {
-        int32_t wsum = 0;
-        if (BITS == 8) {
-#pragma unroll
-            for (int s = 0; s < KS; ++s)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const uint32_t d = (uint32_t)A[s][i];
-                    wsum += (int)(int8_t)d + (int)(int8_t)(d >> 8) + (int)(int8_t)(d >> 16) + (int)(int8_t)(d >> 24);
-                }
-            wsum += __shfl_xor(wsum, 32, 64);  // the other lane half's share of the channel
-        }
-        if constexpr (stair) {
-            // staircase (Eq. (4)): the thresholds moved onto the scaled
-            // accumulator, S (tau - bias) clamped to int32 (stair_thresholds)
-            __align__(16) int32_t T16[16];
-            stair_thresholds(live ? a.thresh + (size_t)ch * NTH : nullptr, NTH, p_bias, SL, T16);
-            if (h == 0) {
-#pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    sPlan[4 * r32 + k] = make_int4(T16[4 * k], T16[4 * k + 1], T16[4 * k + 2], T16[4 * k + 3]);
-            }
-            // every channel's thresholds non-decreasing (the scaling and the
-            // clamp keep their order): the comparison tree applies
-            bool sorted = true;
-#pragma unroll
-            for (int k = 0; k + 1 < NTH; ++k)
-                sorted = sorted && T16[k] <= T16[k + 1];
-            const bool vs = __all(sorted);
-            if (lane == 0)
-                *sVote = vs ? 8 : 0;
-        } else {
-            int4 q0, q1;
-            int64_t b = p_bias;
-            if (BITS == 8)
-                b += 128 * (int64_t)wsum;
-            const int sh = p_shift < 0 ? 0 : (p_shift > 62 ? 62 : p_shift);
-            requant_plan(b, p_mult, sh, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, SL, q0, q1);
-            const bool v3 = __all(!live || q1.z == 3);
-            const bool v34 = __all(!live || q1.z == 3 || q1.z == 4);
-            const bool vm = __all(!live || q1.z != 0 || q0.z > 0);
-            if (h == 0) {
-                sPlan[r32] = q0;
-                sPlan[32 + r32] = q1;
-            }
-            if (lane == 0)
-                *sVote = (v3 ? 1 : 0) | (v34 ? 2 : 0) | (vm ? 4 : 0);
-        }
-    }
-
+    if (!early_plans && wv == 0)
+        compute_plans();
 
     const bool st_ok = live && (r32 % (8 / BITS)) == 0;
     const int ch_byte = gy * 4 * BITS + ((r32 * BITS) >> 3);
