@@ -451,14 +451,31 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     // 64-bit strict form; every channel's code non-decreasing in the
     // accumulator (positive multiplier).  Computed by wave 0 (whose lanes hold
     // the same 32 channels as every wave's) and shared through LDS (read
-    // after the first staging barrier).  Sub-byte plans need no filter sums:
-    // wave 0 computes them before the filter staging, which the other waves
-    // do; 8-bit plans follow the filter fragments, while the other waves
-    // stage the first step ----
+    // after the first staging barrier).  Sub-byte plans need no filter sums
+    // and 8-bit ones of 16-byte filter units read theirs from the filter
+    // rows: wave 0 computes them before the filter staging, which the other
+    // waves do; the remaining 8-bit plans (one-word pixels) follow the
+    // filter fragments, while the other waves stage the first step ----
     v4i A[KS];
     auto compute_plans = [&]() {
         int32_t wsum = 0;
-        if (BITS == 8) {
+        if (BITS == 8 && G::CHUNK) {
+            // the channel's filter sum straight from its row: lane half h
+            // adds the 16-byte units h, h + 2, ... (four bytes per dot
+            // product with ones)
+            if (live) {
+                const uint4 *wr = (const uint4 *)(a.w + (size_t)ch * WROW);
+#pragma unroll
+                for (int u = 0; u < KS; ++u) {
+                    const uint4 v = wr[2 * u + h];
+                    wsum = __builtin_amdgcn_sdot4((int)v.x, 0x01010101, wsum, false);
+                    wsum = __builtin_amdgcn_sdot4((int)v.y, 0x01010101, wsum, false);
+                    wsum = __builtin_amdgcn_sdot4((int)v.z, 0x01010101, wsum, false);
+                    wsum = __builtin_amdgcn_sdot4((int)v.w, 0x01010101, wsum, false);
+                }
+            }
+            wsum += __shfl_xor(wsum, 32, 64);  // the other lane half's share of the channel
+        } else if (BITS == 8) {
 #pragma unroll
             for (int s = 0; s < KS; ++s)
 #pragma unroll
@@ -505,7 +522,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 *sVote = (v3 ? 1 : 0) | (v34 ? 2 : 0) | (vm ? 4 : 0);
         }
     };
-    constexpr bool early_plans = BITS != 8;
+    constexpr bool early_plans = BITS != 8 || G::CHUNK;
     if (early_plans && wv == 0)
         compute_plans();
     if constexpr (G::CHUNK) {
