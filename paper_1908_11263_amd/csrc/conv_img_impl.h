@@ -308,6 +308,37 @@ __device__ __forceinline__ uint32_t stair_tree(int32_t acc, const int32_t *T)
     }
 }
 
+// The same tree with its last two levels' thresholds read from the lane's
+// threshold column in LDS (T[i] at col[32 i]: the 32 lanes of a half-wave
+// read 32 consecutive words, one per bank), at the index the bits decided so
+// far give: for 15 thresholds the code is built one bit per comparison and
+// only T[3], T[7] and T[11] are held in registers.
+// 2 x + (acc >= t): the comparison's result is the carry into the add (two
+// instructions; written out because the compiler builds the bit with a select
+// and an or).  Only vcc, a vector-written lane mask, is clobbered.
+__device__ __forceinline__ uint32_t stair_bit(uint32_t x, int32_t acc, int32_t t)
+{
+    uint32_t r;
+    __asm__("v_cmp_ge_i32_e32 vcc, %1, %2\n\tv_addc_co_u32_e32 %0, vcc, %3, %3, vcc"
+            : "=v"(r)
+            : "v"(acc), "v"(t), "v"(x)
+            : "vcc");
+    return r;
+}
+
+template <int NT>
+__device__ __forceinline__ uint32_t stair_tree_col(int32_t acc, const int32_t *T, const int32_t *col)
+{
+    if constexpr (NT == 15) {
+        uint32_t x = acc >= T[7] ? 1u : 0u;                      // count >= 8
+        x = stair_bit(x, acc, x ? T[11] : T[3]);                 // q: count >= 4 q
+        x = stair_bit(x, acc, col[32 * (4 * x + 1)]);            // count >= 4 q + 2
+        return stair_bit(x, acc, col[32 * (2 * x)]);             // count >= 4 q + 2 c1 + 1
+    } else {
+        return stair_tree<NT>(acc, T);
+    }
+}
+
 // A compile-time int (the byte stride of an output pixel in the store fast
 // paths).
 template <int V>
@@ -409,15 +440,23 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     int grp = blockIdx.x;
     if (grp < a.ngroups)
         issue(grp);
-    // the channel parameters of the plans (wave 0), loaded now so that their
-    // latency overlaps the image and filter loads
+    // the channel parameters of the plans (wave 0: bias, multiplier and
+    // shift, or the staircase thresholds), loaded now so that their latency
+    // overlaps the image and filter loads
     int32_t p_bias = 0, p_mult = 0, p_shift = 0;
+    constexpr int NTH = (1 << BITS) - 1;  // staircase thresholds per channel (4 and 2 bits)
+    int32_t p_tau[STAIR ? NTH : 1];
     if (wv == 0 && live) {
         if (a.bias)
             p_bias = a.bias[ch];
         if (a.epi == EPI_REQUANT) {
             p_mult = a.mult[ch];
             p_shift = a.shift[ch];
+        }
+        if constexpr (STAIR) {
+#pragma unroll
+            for (int k = 0; k < NTH; ++k)
+                p_tau[k] = a.thresh[(size_t)ch * NTH + k];
         }
     }
 
@@ -427,12 +466,11 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     // group's compression plans and fast-path votes
     uint8_t *sF = smem + (size_t)a.ipw * a.tile_bytes;
     // the requantization plans (e0 of the 32 channels, then their e1: lanes
-    // read consecutive 16-byte entries), or [32 channels][16] staircase
+    // read consecutive 16-byte entries), or [16][32 channels] staircase
     // thresholds on the kernel's accumulator scale
     int4 *sPlan = (int4 *)(sF + G::FLDS);
     int *sVote = (int *)(sPlan + 128);
     uint8_t *sOut = (uint8_t *)(sPlan + 129) + wv * 64 * G::OPS;  // this wave's output staging
-    constexpr int NTH = (1 << BITS) - 1;  // staircase thresholds per channel (4 and 2 bits)
     // STAIR instances compute only the staircase (Eq. (4)); the others every
     // other epilogue (a separate instance keeps each one's code small)
     constexpr bool stair = STAIR;
@@ -489,11 +527,11 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             // staircase (Eq. (4)): the thresholds moved onto the scaled
             // accumulator, S (tau - bias) clamped to int32 (stair_thresholds)
             __align__(16) int32_t T16[16];
-            stair_thresholds(live ? a.thresh + (size_t)ch * NTH : nullptr, NTH, p_bias, SL, T16);
+            stair_thresholds(live ? p_tau : nullptr, NTH, p_bias, SL, T16);
             if (h == 0) {
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    sPlan[4 * r32 + k] = make_int4(T16[4 * k], T16[4 * k + 1], T16[4 * k + 2], T16[4 * k + 3]);
+                for (int k = 0; k < 16; ++k)
+                    ((int32_t *)sPlan)[32 * k + r32] = T16[k];
             }
             // every channel's thresholds non-decreasing (the scaling and the
             // clamp keep their order): the comparison tree applies
@@ -705,12 +743,13 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             }
         };
         // the lane's staircase thresholds (read per step: registers only in
-        // the staircase epilogue)
+        // the staircase epilogue) from its column of the threshold-major
+        // table (T[k] of the 32 channels at words 32 k ..)
+        const int32_t *stair_col = (const int32_t *)sPlan + r32;
         auto stair_T = [&](int32_t *T) {
-            const int32_t *src = (const int32_t *)(sPlan + 4 * r32);
 #pragma unroll
             for (int k = 0; k < NTH; ++k)
-                T[k] = src[k];
+                T[k] = stair_col[32 * k];
         };
         // ---- epilogues: lane (r32, h) holds channel ch for tile pixels
         // p = 8*(v/4) + 4h + v%4 (register v): image row T*RT + p/WOP,
@@ -793,7 +832,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                             int32_t x0, x1, y0, y1;
                             win(k, c0, c1, x0, x1, y0, y1);
                             const int32_t mx = max(max(x0, x1), max(y0, y1));
-                            code[k] = decltype(tree)::value ? stair_tree<NTH>(mx, T) : stair_level<NTH>(mx, T);
+                            code[k] = decltype(tree)::value ? stair_tree_col<NTH>(mx, T, stair_col) : stair_level<NTH>(mx, T);
                         }
                         store_pool(img, orow, hx, code);
                     });
@@ -929,8 +968,8 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
 #pragma unroll
                         for (int v = 0; v < 16; ++v) {
                             if (decltype(tree)::value) {
-                                code[v] = stair_tree<NTH>(c0[v], T);
-                                code[16 + v] = stair_tree<NTH>(c1[v], T);
+                                code[v] = stair_tree_col<NTH>(c0[v], T, stair_col);
+                                code[16 + v] = stair_tree_col<NTH>(c1[v], T, stair_col);
                             } else {
                                 code[v] = stair_level<NTH>(c0[v], T);
                                 code[16 + v] = stair_level<NTH>(c1[v], T);
