@@ -326,3 +326,35 @@ def test_img_stair_unsorted(qnn, orc):
         if L.ho >= 2 and L.wo >= 2:
             check(qnn, orc, L, pool=True)
 
+
+
+def test_img_stair_ties_and_extremes(qnn, orc):
+    """Sorted thresholds with ties (every odd threshold equal to its left
+    neighbour) and thresholds far outside the accumulator range, whose
+    scaled form clamps to the int32 limits: a channel whose thresholds all
+    lie below every accumulator (code 2^b - 1 throughout), one whose
+    thresholds all lie above (code 0), and random runs of extremes at both
+    ends of the others.  The comparison tree must count exactly at equal
+    thresholds and at the clamped ends."""
+    import dataclasses
+    lo, hi = -(1 << 31), (1 << 31) - 1
+    cases = [(4, 64, 2, 32, 32, 64, 3, 1), (4, 64, 1, 12, 9, 40, 3, 1), (2, 64, 2, 9, 16, 32, 3, 1)]
+    for i, (bits, c, n, h, w, m, k, pad) in enumerate(cases):
+        L = stair_img_layer(bits, c, n, h, w, m, k, pad, seed=800 + i)
+        rng = np.random.default_rng(900 + i)
+        t = L.thresh.astype(np.int64)
+        t[:, 1::2] = t[:, 0:-1:2]
+        nt = t.shape[1]
+        for j in range(2, m):
+            r, s = rng.integers(0, 3), rng.integers(0, 4)
+            t[j, :r] = lo
+            if s:
+                t[j, nt - s:] = hi
+        t[0, :] = lo
+        t[1, :] = hi
+        t = np.sort(t, axis=1)
+        L2 = dataclasses.replace(L, name=L.name + "_ties", thresh=t.astype(np.int32))
+        check(qnn, orc, L2, tile=IMAGE)
+        check(qnn, orc, L2)
+        if L2.ho >= 2 and L2.wo >= 2:
+            check(qnn, orc, L2, pool=True)
