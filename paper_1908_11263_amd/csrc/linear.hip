@@ -81,18 +81,31 @@ __global__ void __launch_bounds__(256) linear_raw_kernel(const uint8_t *__restri
     const uint8_t *wr = w + (size_t)(win ? ch : 0) * kb + kq * FB;
     v4i acc = {0, 0, 0, 0};
     int wsum = 0;
-    // wave wv takes K steps wv, wv + 4, ...: 64 values each, 16 per lane group
-    for (int s = wv; s < ksteps; s += 4) {
-        const v4i a = lin_frag<BITS, false>(xr + (size_t)s * 4 * FB, xin);
-        const v4i b = lin_frag<BITS, true>(wr + (size_t)s * 4 * FB, win);
+    // wave wv takes K steps wv, wv + 4, ...: 64 values each, 16 per lane
+    // group; four of its steps at a time have all their loads issued before
+    // their products (one memory round trip per four steps)
+    auto step = [&](const v4i &a, const v4i &b) {
         if (BITS == 8) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                wsum += (int)(int8_t)b[i] + (int)(int8_t)(b[i] >> 8) + (int)(int8_t)(b[i] >> 16) +
-                        (int)(int8_t)(b[i] >> 24);
+                wsum = __builtin_amdgcn_sdot4((int)b[i], 0x01010101, wsum, false);
         }
         acc = __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, acc, 0, 0, 0);
+    };
+    int s = wv;
+    for (; s + 12 < ksteps; s += 16) {
+        v4i fa[4], fb[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            fa[u] = lin_frag<BITS, false>(xr + (size_t)(s + 4 * u) * 4 * FB, xin);
+            fb[u] = lin_frag<BITS, true>(wr + (size_t)(s + 4 * u) * 4 * FB, win);
+        }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            step(fa[u], fb[u]);
     }
+    for (; s < ksteps; s += 4)
+        step(lin_frag<BITS, false>(xr + (size_t)s * 4 * FB, xin), lin_frag<BITS, true>(wr + (size_t)s * 4 * FB, win));
     // lane l holds channel l%16 for images 4*(l/16) + i
 #pragma unroll
     for (int i = 0; i < 4; ++i)
