@@ -31,15 +31,15 @@ __global__ void __launch_bounds__(256) conv_xnor_kernel(const uint32_t *__restri
 #pragma unroll
         for (int i = 0; i < 32; ++i)
             pop[i] = 0;
-        const uint32_t *wg = wgl + grp * 32 * a.kd;
+        const uint32_t *wg = wgl + (size_t)grp * 32 * a.kd;
         const int nvalid = min(32, a.m - grp * 32);
         for (int ky = 0; ky < a.kh; ++ky) {
             const int iy = oy * a.sh - a.ph + ky;
             for (int kx = 0; kx < a.kw; ++kx) {
                 const int ix = ox * a.sw - a.pw + kx;
                 const bool in = iy >= 0 && iy < a.h && ix >= 0 && ix < a.w_;
-                const uint32_t *xp = xg + ((n * a.h + (in ? iy : 0)) * a.w_ + (in ? ix : 0)) * a.cd;
-                const uint32_t *wt = wg + (ky * a.kw + kx) * a.cd;
+                const uint32_t *xp = xg + ((size_t)(n * a.h + (in ? iy : 0)) * a.w_ + (in ? ix : 0)) * a.cd;
+                const uint32_t *wt = wg + (size_t)(ky * a.kw + kx) * a.cd;
                 for (int d0 = 0; d0 < a.cd; d0 += KB) {
                     uint32_t xv[KB];
 #pragma unroll
@@ -50,14 +50,14 @@ __global__ void __launch_bounds__(256) conv_xnor_kernel(const uint32_t *__restri
                         for (int mm = 0; mm < 32; ++mm)
 #pragma unroll
                             for (int d = 0; d < KB; ++d)
-                                pop[mm] += __popc(~(xv[d] ^ wt[mm * a.kd + d0 + d]));
+                                pop[mm] += __popc(~(xv[d] ^ wt[(size_t)mm * a.kd + d0 + d]));
                     } else {
 #pragma unroll
                         for (int mm = 0; mm < 32; ++mm) {
                             if (mm < nvalid) {
 #pragma unroll
                                 for (int d = 0; d < KB; ++d)
-                                    pop[mm] += __popc(~(xv[d] ^ wt[mm * a.kd + d0 + d]));
+                                    pop[mm] += __popc(~(xv[d] ^ wt[(size_t)mm * a.kd + d0 + d]));
                             }
                         }
                     }
@@ -161,7 +161,7 @@ __global__ void __launch_bounds__(256) conv_xnor_res_kernel(const uint32_t *__re
             const int iy = oy * a.sh - a.ph + ky, ix = ox * a.sw - a.pw + kx;
             xv[k] = 0u;
             if (iy >= 0 && iy < a.h && ix >= 0 && ix < a.w_)
-                xv[k] = xg[((n * a.h + iy) * a.w_ + ix) * a.cd + d];
+                xv[k] = xg[((size_t)(n * a.h + iy) * a.w_ + ix) * a.cd + d];
         }
     }
 

@@ -12,6 +12,9 @@ EPI = {"requant": 0, "thresh1": 1, "raw32": 2, "stair": 3}
 
 
 def threads():
+    """Oracle threads: the host cores available, at most 16 (the CPU share
+    that goes with one GPU on a shared GPU host; more threads there would
+    take cores from other jobs' processes)."""
     try:
         n = len(os.sched_getaffinity(0))
     except AttributeError:
@@ -42,22 +45,31 @@ def gpu_conv(L, epi=None, stream=None):
     return y.cpu().numpy()
 
 
-def oracle_conv(orc, L, epi=None, images=None):
-    """Oracle output of layer L (optionally for a subset of images)."""
+# whole oracle outputs of the large workloads, kept for the session: the
+# integer and the FP4 paths of a layer are both compared with one oracle run
+_ORACLE_CACHE = {}
+
+
+def oracle_conv(orc, L, epi=None):
+    """Oracle output of layer L (the whole batch); outputs of layers of more
+    than 2^28 MACs are cached per (input digest, epilogue)."""
     epi = epi or L.epi
-    x = L.x if images is None else L.x[images]
-    n = x.shape[0]
-    _, y = orc.conv2d(x, (n, L.h, L.w, L.c), L.bits, L.wt, L.m, L.kh, L.kw, L.stride, L.pad,
+    key = (L.name, L.digest(), epi)
+    if key in _ORACLE_CACHE:
+        return _ORACLE_CACHE[key]
+    _, y = orc.conv2d(L.x, (L.n, L.h, L.w, L.c), L.bits, L.wt, L.m, L.kh, L.kw, L.stride, L.pad,
                       EPI[epi], L.bias, L.mult, L.shift, L.thresh, L.clip, nthreads=threads())
+    if L.macs > (1 << 28):
+        _ORACLE_CACHE[key] = y
     return y
 
 
-def sample_images(n, k=6, seed=0):
-    """First, last and a few random images of a batch (full-size checks)."""
-    rng = np.random.default_rng(seed)
-    idx = {0, n - 1}
-    idx.update(rng.integers(0, n, size=k).tolist())
-    return np.array(sorted(idx))
+def compare(got, want, what):
+    """Byte-for-byte equality of two outputs, naming the first mismatches."""
+    assert got.shape == want.shape, "%s: shape %s, oracle %s" % (what, got.shape, want.shape)
+    bad = np.argwhere(got != want)
+    assert bad.size == 0, "%s: %d mismatches of %d, first at %s" % (
+        what, len(bad), got.size, bad[:5].tolist())
 
 
 def with_epi(L, epi):

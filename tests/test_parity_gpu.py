@@ -4,8 +4,7 @@ import numpy as np
 import pytest
 
 import synth
-from gpu_helpers import (dev, distribution, gpu_conv, log, oracle_conv, sample_images, threads,
-                         with_epi)
+from gpu_helpers import compare, dev, distribution, gpu_conv, log, oracle_conv, threads, with_epi
 
 pytestmark = pytest.mark.gpu
 
@@ -20,17 +19,13 @@ def qnn():
     return q
 
 
-def check_layer(orc, L, epi=None, images=None):
+def check_layer(orc, L, epi=None):
+    """The whole output of layer L on the GPU against the oracle's."""
     epi = epi or L.epi
     log("case", L.name, epi, "N=%d H=%d W=%d C=%d M=%d k=%dx%d s=%s p=%s bits=%d" % (
         L.n, L.h, L.w, L.c, L.m, L.kh, L.kw, L.stride, L.pad, L.bits))
     got = gpu_conv(L, epi)
-    want = oracle_conv(orc, L, epi, images)
-    if images is not None:
-        got = got[images]
-    assert got.shape == want.shape
-    bad = np.argwhere(got != want)
-    assert bad.size == 0, "%s: %d mismatches, first at %s" % (L.name, len(bad), bad[:5].tolist())
+    compare(got, oracle_conv(orc, L, epi), "%s %s" % (L.name, epi))
     return got
 
 
@@ -46,7 +41,7 @@ def test_int8_layer_batch1(qnn, orc):
 def test_int4_layer_batch64(qnn, orc):
     L = synth.int4_layer()
     check_layer(orc, L)
-    check_layer(orc, with_epi(L, "raw32"), images=sample_images(L.n))
+    check_layer(orc, with_epi(L, "raw32"))
     C = synth.centred(L)
     y = check_layer(orc, C)
     z, top = distribution(y, 4)
@@ -56,10 +51,10 @@ def test_int4_layer_batch64(qnn, orc):
 
 def test_int2_layer_batch256(qnn, orc):
     L = synth.int2_layer()
-    check_layer(orc, L, images=sample_images(L.n))
-    check_layer(orc, with_epi(L, "raw32"), images=sample_images(L.n, seed=1))
+    check_layer(orc, L)
+    check_layer(orc, with_epi(L, "raw32"))
     C = synth.centred(L)
-    y = check_layer(orc, C, images=sample_images(L.n, seed=2))
+    y = check_layer(orc, C)
     z, top = distribution(y, 2)
     log("int2 centred distribution (zero, top):", z, top)
     assert 0.2 < z < 0.8
@@ -67,14 +62,18 @@ def test_int2_layer_batch256(qnn, orc):
 
 def test_int1_layer_batch1024(qnn, orc):
     L = synth.int1_layer()
-    check_layer(orc, L, images=sample_images(L.n))
-    check_layer(orc, with_epi(L, "raw32"), images=sample_images(L.n, seed=3))
+    check_layer(orc, L)
+    check_layer(orc, with_epi(L, "raw32"))
 
 
-def oracle_network(orc, net, images):
-    x = net.packed_input()[images]
+def oracle_network(orc, net):
+    """The network on the oracle, layer by layer (convolution, then
+    max-pooling), over the whole batch: (logits [n, 10], pooled activations
+    of each layer)."""
+    x = net.packed_input()
     n = x.shape[0]
     h, c = 32, x.shape[-1] * 8 // net.bits
+    acts = []
     for cv in net.convs:
         wt = synth.pack_codes(synth.to_code(cv["w_vals"], net.bits, True).reshape(cv["m"], -1),
                               net.bits)
@@ -82,13 +81,15 @@ def oracle_network(orc, net, images):
                           cv["bias"], cv["mult"], cv["shift"], None, net.clip, nthreads=threads())
         c = cv["m"]
         x = orc.maxpool2d(y, (n, h, h, c), net.bits, 2, 2, 2, 2)
+        acts.append(x)
         h //= 2
     fcw = synth.pack_codes(synth.to_code(net.fc_w_vals, net.bits, True), net.bits)
     _, logits = orc.linear(x, n, h * h * c, net.bits, fcw, 10, epi=2, bias=net.fc_bias)
-    return logits
+    return logits, acts
 
 
 def gpu_network(qnn, net, fused=True):
+    """The network on the GPU: (logits [n, 10], the layers' pooled outputs)."""
     import torch
     from paper_1908_11263_amd.network import cifar_forward
     convs = []
@@ -101,28 +102,34 @@ def gpu_network(qnn, net, fused=True):
               bias=dev(net.fc_bias), m=10)
     x = dev(net.packed_input())
     cin = net.x_vals.shape[-1]
-    logits = cifar_forward(x, net.n, net.bits, cin, convs, fc, net.clip, fused=fused)
+    logits, acts = cifar_forward(x, net.n, net.bits, cin, convs, fc, net.clip, fused=fused,
+                                 keep=True)
     torch.cuda.synchronize()
-    return logits.cpu().numpy().reshape(net.n, 10)
+    pooled = acts if fused else acts[1::2]
+    return logits.cpu().numpy().reshape(net.n, 10), [a.cpu().numpy() for a in pooled]
+
+
+def check_network(qnn, orc, net, fused=True):
+    log("case cifar network bits=%d N=%d fused=%s" % (net.bits, net.n, fused))
+    want, want_acts = oracle_network(orc, net)
+    got, got_acts = gpu_network(qnn, net, fused=fused)
+    for i, (g, w) in enumerate(zip(got_acts, want_acts)):
+        compare(g, w, "cifar%d layer %d (conv + pool)" % (net.bits, i + 1))
+    compare(got, want, "cifar%d logits" % net.bits)
 
 
 @pytest.mark.parametrize("bits", [8, 4])
 def test_cifar_network_small_batch(qnn, orc, bits):
     net = synth.cifar_network(bits=bits, n=5)
-    log("case cifar network bits=%d N=5" % bits)
-    want = oracle_network(orc, net, np.arange(5))
-    assert np.array_equal(gpu_network(qnn, net), want)
-    assert np.array_equal(gpu_network(qnn, net, fused=False), want)
+    check_network(qnn, orc, net)
+    check_network(qnn, orc, net, fused=False)
 
 
 @pytest.mark.parametrize("bits", [8, 4])
-def test_cifar_network_batch4096_sampled(qnn, orc, bits):
-    net = synth.cifar_network(bits=bits, n=4096)
-    log("case cifar network bits=%d N=4096" % bits)
-    got = gpu_network(qnn, net)
-    idx = sample_images(net.n, k=4, seed=bits)
-    want = oracle_network(orc, net, idx)
-    assert np.array_equal(got[idx], want)
+def test_cifar_network_batch4096(qnn, orc, bits):
+    """The whole batch-4096 network: every layer's pooled output and the
+    logits of every image against the oracle."""
+    check_network(qnn, orc, synth.cifar_network(bits=bits, n=4096))
 
 
 # ------------------------------------------------------ random small layers
@@ -206,9 +213,11 @@ def test_linear(qnn, orc, bits):
     import torch
     rng = np.random.default_rng(90 + bits)
     # K a multiple of 64 (the fully connected kernel) with ragged image and
-    # channel counts, and K = 96 at 8 bits (the convolution tiles)
+    # channel counts, and K = 96 at 8 bits (the convolution tiles); 20 and 21
+    # K steps of 64 run the four-step block and then the remainder loop
     for (n, h, w, c, m) in [(37, 4, 4, 64, 10), (5, 1, 1, 1024, 10), (9, 2, 3, 32 * 4 // bits, 33),
-                            (300, 4, 4, 128, 70), (16, 1, 1, 4096, 16), (33, 8, 8, 64, 1)]:
+                            (300, 4, 4, 128, 70), (16, 1, 1, 4096, 16), (33, 8, 8, 64, 1),
+                            (19, 1, 1, 64 * 20, 12), (19, 1, 1, 64 * 21, 10)]:
         if bits == 1:
             xv = 2 * rng.integers(0, 2, size=(n, h, w, c)) - 1
             wv = 2 * rng.integers(0, 2, size=(m, h * w * c)) - 1

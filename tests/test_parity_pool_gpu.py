@@ -5,7 +5,7 @@ import numpy as np
 import pytest
 
 import synth
-from gpu_helpers import EPI, dev, log, sample_images, threads
+from gpu_helpers import EPI, compare, dev, log, threads
 
 pytestmark = pytest.mark.gpu
 
@@ -29,24 +29,18 @@ def gpu_pool(qnn, L):
     return y.cpu().numpy()
 
 
-def oracle_pool(orc, L, images=None):
-    x = L.x if images is None else L.x[images]
-    n = x.shape[0]
-    _, y = orc.conv2d(x, (n, L.h, L.w, L.c), L.bits, L.wt, L.m, L.kh, L.kw, L.stride, L.pad,
+def oracle_pool(orc, L):
+    n = L.n
+    _, y = orc.conv2d(L.x, (n, L.h, L.w, L.c), L.bits, L.wt, L.m, L.kh, L.kw, L.stride, L.pad,
                       EPI[L.epi], L.bias, L.mult, L.shift, L.thresh, L.clip, nthreads=threads())
     return orc.maxpool2d(y, (n, L.ho, L.wo, L.m), L.bits, 2, 2, 2, 2)
 
 
-def check(qnn, orc, L, images=None):
+def check(qnn, orc, L):
     log("case", L.name, L.epi, "pool N=%d H=%d W=%d C=%d M=%d k=%d s=%s p=%s bits=%d" % (
         L.n, L.h, L.w, L.c, L.m, L.kh, L.stride, L.pad, L.bits))
     got = gpu_pool(qnn, L)
-    want = oracle_pool(orc, L, images)
-    if images is not None:
-        got = got[images]
-    assert got.shape == want.shape, (got.shape, want.shape)
-    bad = np.argwhere(got != want)
-    assert bad.size == 0, "%s: %d mismatches, first at %s" % (L.name, len(bad), bad[:5].tolist())
+    compare(got, oracle_pool(orc, L), "%s %s pool" % (L.name, L.epi))
     return got
 
 
@@ -93,16 +87,16 @@ def test_pool_staircase(qnn, orc, bits):
     unit = 32 // bits
     for (n, h, w, m) in [(2, 9, 8, 12), (24, 32, 32, 64)]:
         L = layer(bits, n, h, w, 2 * unit, m, 3, seed=m, epi="stair")
-        check(qnn, orc, L, images=None if n < 4 else sample_images(n, k=3, seed=2))
+        check(qnn, orc, L)
 
 
 @pytest.mark.parametrize("bits", [8, 4])
 def test_pool_cifar_layers_batch4096(qnn, orc, bits):
     """The three conv + pool layers of the CIFAR-shaped network at batch 4096
-    (sampled images), fused, against the oracle."""
+    (whole outputs), fused, against the oracle; the later layers on random
+    codes over the whole code range."""
     net = synth.cifar_network(bits=bits, n=4096)
     hw = 32
-    idx = sample_images(net.n, k=3, seed=bits)
     rng = np.random.default_rng(17)
     for i, cv in enumerate(net.convs):
         if i == 0:
@@ -112,5 +106,5 @@ def test_pool_cifar_layers_batch4096(qnn, orc, bits):
         L = synth.ConvLayer("cifar%d_conv%d" % (bits, i + 1), bits, net.n, hw, hw, cv["c"], cv["m"],
                             5, 5, (1, 1), (2, 2), "requant", x_vals, cv["w_vals"], cv["bias"],
                             cv["mult"], cv["shift"], None, net.clip, cv["c_alg"])
-        check(qnn, orc, L, images=idx)
+        check(qnn, orc, L)
         hw //= 2

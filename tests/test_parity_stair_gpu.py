@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import synth
-from gpu_helpers import gpu_conv, log, oracle_conv, sample_images, with_epi
+from gpu_helpers import compare, gpu_conv, log, oracle_conv, with_epi
 
 pytestmark = pytest.mark.gpu
 
@@ -21,15 +21,11 @@ def qnn():
     return q
 
 
-def check(orc, L, images=None):
+def check(orc, L):
     log("case", L.name, "stair N=%d H=%d W=%d C=%d M=%d k=%d bits=%d" % (
         L.n, L.h, L.w, L.c, L.m, L.kh, L.bits))
     got = gpu_conv(L)
-    want = oracle_conv(orc, L, images=images)
-    if images is not None:
-        got = got[images]
-    bad = np.argwhere(got != want)
-    assert bad.size == 0, "%s: %d mismatches, first at %s" % (L.name, len(bad), bad[:5].tolist())
+    compare(got, oracle_conv(orc, L), L.name)
     return got
 
 
@@ -69,8 +65,7 @@ def test_stair_both_kernels_ragged_channels(qnn, orc, bits):
         # few tiles: the 16x16 kernel
         check(orc, stair_layer(bits, 2, 7, 9, 2 * unit, m, 3, seed=m))
         # enough tiles for the 32x32 kernel when m >= 32
-        check(orc, stair_layer(bits, 24, 32, 32, 2 * unit, m, 3, seed=100 + m),
-              images=sample_images(24, k=3, seed=m))
+        check(orc, stair_layer(bits, 24, 32, 32, 2 * unit, m, 3, seed=100 + m))
 
 
 @pytest.mark.parametrize("bits", [4, 2])
@@ -79,14 +74,14 @@ def test_stair_unsorted_thresholds(qnn, orc, bits):
     for (n, h, w, m) in ((2, 6, 5, 20), (24, 32, 32, 64)):
         L = stair_layer(bits, n, h, w, 2 * unit, m, 3, seed=7 * m, sorted_=False)
         assert (np.diff(L.thresh, axis=1) < 0).any()
-        check(orc, L, images=None if n < 4 else sample_images(n, k=3, seed=1))
+        check(orc, L)
 
 
 @pytest.mark.parametrize("which", ["int4", "int2"])
 def test_stair_with_derived_thresholds_equals_requant(qnn, orc, which):
     """A workload layer (centred bias) run with the thresholds of its own
     multiplier/shift: the staircase output equals the requantized output, on
-    the GPU, and both equal the oracle on sampled images."""
+    the GPU, and the staircase output equals the oracle's."""
     L = synth.centred(synth.int4_layer() if which == "int4" else synth.int2_layer())
     hi = (1 << L.bits) - 1
     assert L.clip == (0, hi)
@@ -95,8 +90,7 @@ def test_stair_with_derived_thresholds_equals_requant(qnn, orc, which):
     S = with_epi(L, "stair")
     S.thresh = tau.astype(np.int32)
     got_req = gpu_conv(L)
-    idx = sample_images(L.n, k=3, seed=5)
-    got = check(orc, S, images=idx)
+    got = check(orc, S)
     assert np.array_equal(gpu_conv(S), got_req)
     del got
 
@@ -120,6 +114,6 @@ def test_stair_extreme_thresholds(qnn, orc):
 def test_stair_bench_workload(qnn, orc):
     """The benchmarked staircase layer (INT4, batch 64, 32x32x64 -> 64)."""
     L = synth.int4_stair_layer()
-    y = check(orc, L, images=sample_images(L.n, k=4, seed=11))
+    y = check(orc, L)
     codes = np.concatenate([(y & 15).ravel(), (y >> 4).ravel()])
     log("int4 stair codes: min %d max %d distinct %d" % (codes.min(), codes.max(), len(np.unique(codes))))
