@@ -28,6 +28,40 @@ def test_exports_every_header_function(q, L):
     assert L.qnn_abi_version() == 7
 
 
+def test_exports_every_calibration_function(q, L):
+    """The measurement entry points (include/qnn_calib.h) are exported and
+    refuse bad arguments on the host, before any device call."""
+    import os
+    import re
+    path = os.path.join(os.path.dirname(q.qnn.HEADER), "qnn_calib.h")
+    with open(path) as f:
+        text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+    names = sorted(set(re.findall(r"\b(qnn_calib_[a-z0-9_]+)\s*\(", text)))
+    assert names == ["qnn_calib_copy", "qnn_calib_empty", "qnn_calib_mfma_i8", "qnn_calib_xnor"]
+    for name in names:
+        assert hasattr(L, name), name
+    P, i32 = ctypes.c_void_p, ctypes.c_int32
+    for name in ("qnn_calib_mfma_i8", "qnn_calib_xnor"):
+        f = getattr(L, name)
+        f.restype = ctypes.c_int
+        f.argtypes = [i32, i32, P, P, P]
+        assert f(4, 10, None, None, None) == 1                 # NULL output
+        assert f(0, 10, P(4096), None, None) == 4              # no workgroups
+        assert f(1 << 21, 10, P(4096), None, None) == 4        # too many
+        assert f(4, 0, P(4096), None, None) == 4               # no iterations
+        assert f(4, 10, P(4100), None, None) == 5              # misaligned output
+        assert f(4, 10, P(4096), P(4104), None) == 5           # misaligned clock buffer
+    L.qnn_calib_copy.restype = ctypes.c_int
+    L.qnn_calib_copy.argtypes = [P, P, ctypes.c_size_t, P]
+    assert L.qnn_calib_copy(None, P(4096), 16, None) == 1
+    assert L.qnn_calib_copy(P(4096), P(8192), 17, None) == 5   # not whole quads
+    assert L.qnn_calib_copy(P(4096), P(4112), 32, None) == 4   # overlapping
+    assert L.qnn_calib_copy(P(4096), P(8192), 1 << 41, None) == 3
+    L.qnn_calib_empty.restype = ctypes.c_int
+    L.qnn_calib_empty.argtypes = [i32, P]
+    assert L.qnn_calib_empty(0, None) == 4
+
+
 def test_status_strings(q, L):
     for code in range(10):
         assert L.qnn_status_string(code)
