@@ -86,7 +86,12 @@ template <int BITS, int P, int KH, int KW, int WOP>
 struct ImgGeom {
     static constexpr int U = P * 8 / BITS;             // unpacked bytes per pixel
     static constexpr bool CHUNK = U >= 32;             // K split by 16-byte halves of 32-byte chunks
-    static constexpr int SB = U == 4 ? 8 : U;          // tile slot bytes (8-bit one-word pixels: a pair)
+    // tile slot bytes: 8-bit one-word pixels a pair; pixels of 32 unpacked
+    // bytes or more one pixel and 16 bytes of padding (an odd number of
+    // 16-byte units apart, the 16-byte im2col reads of 8 neighbouring lanes
+    // fall in 8 different bank quads; with slots a power of two apart they
+    // hit 2 or 4 times the same banks)
+    static constexpr int SB = U == 4 ? 8 : (U >= 32 ? U + 16 : U);
     static constexpr int PP = WOP + KW - 1;            // tile pitch, slots
     static constexpr int RB = PP * SB;                 // tile row, bytes
     static constexpr int RT = 32 / WOP;                // image rows per MFMA row tile
@@ -203,10 +208,38 @@ __device__ __forceinline__ uint32_t img_code(int32_t accd, const int4 &e0, const
     return (uint32_t)r;
 }
 
+// Mode-3 plans whose clamp interval lies in the signed 24-bit range (every
+// channel's code fits the 32-bit form): with p = (L, H, mult, C) from
+// img_plan3, the code is ((med3(acc, L, H) * mult + C) mod 2^32) >> shift,
+// three instructions.  med3(acc, L, H) - L is the strict form's clamped
+// difference and C = n0 - L * mult (mod 2^32), so the 32-bit multiply-add
+// wraps to the exact strict-form value, which is below 2^32.  acc must come
+// from an instruction the compiler sees (here: the maximum of a pooling
+// window), not straight from a matrix instruction: the compiler inserts no
+// wait states before an asm reader.
+__device__ __forceinline__ uint32_t img_code3(int32_t accd, const int4 &p, int32_t sh)
+{
+    int32_t x, y;
+    __asm__("v_med3_i32 %0, %1, %2, %3" : "=v"(x) : "v"(accd), "v"(p.x), "v"(p.y));
+    __asm__("v_mad_i32_i24 %0, %1, %2, %3" : "=v"(y) : "v"(x), "v"(p.z), "v"(p.w));
+    return (uint32_t)y >> sh;
+}
+
+// The three-instruction form of a mode-3 plan (e0 = (A, DS, mult, RS), the
+// strict form's clamp base, width, multiplier and rounding term): clamp
+// interval [L, H] = [A, A + DS], C = RS - A * mult mod 2^32; false when L, H
+// or mult leave the signed 24-bit range of v_mad_i32_i24.
+__device__ __forceinline__ bool img_plan3(const int4 &e0, const int4 &e1, int4 &p)
+{
+    const int64_t L = e0.x, H = (int64_t)e0.x + e0.y;
+    p = make_int4(e0.x, (int32_t)H, e0.z, (int32_t)((uint32_t)e0.w - (uint32_t)e0.x * (uint32_t)e0.z));
+    return e1.z == 3 && L >= -(1 << 23) && H < (1 << 23) && e0.z < (1 << 23);
+}
+
 // Mode-3 plans only (every channel's code fits the 32-bit form): a
 // saturating subtract, a median-of-three clamp to [0, e0.y] (e0.y >= 0), a
 // 24-bit multiply-add and a shift.
-__device__ __forceinline__ uint32_t img_code3(int32_t accd, const int4 &e0, const int4 &e1)
+__device__ __forceinline__ uint32_t img_code3s(int32_t accd, const int4 &e0, const int4 &e1)
 {
     const int32_t d = __builtin_elementwise_sub_sat(accd, e0.x);
     int32_t dc;
@@ -389,11 +422,37 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     const int wv = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
     const int gy = blockIdx.y;
     const int ch = gy * 32 + r32;
+    // the kernel arguments read before the first barrier, requested together
+    // (left to itself the compiler waits for one scalar load before issuing
+    // the next: three dependent round trips before the first input load)
+    __asm__ volatile("" ::"s"(a.x), "s"(a.w), "s"(a.bias), "s"(a.mult), "s"(a.shift), "s"(a.h), "s"(a.w_),
+                     "s"(a.m), "s"(a.ph), "s"(a.n), "s"(a.epi), "s"(a.thresh), "s"(a.ipw), "s"(a.tile_bytes),
+                     "s"(a.ngroups), "s"(a.quads), "s"(a.bands), "s"(a.brows), "s"(a.trows),
+                     "s"(a.div_bands.mul), "s"(a.div_bands.shr));
     const bool live = ch < a.m;
     const int npix = a.h * a.w_;
     const int imgq = npix * P / 16;  // 16-byte quads per image (P = 4: with a.quads)
 
-    // ---- the first image group's bytes: issued before anything else ----
+    // the channel parameters of the plans (wave 0: bias, multiplier and
+    // shift, or the staircase thresholds), requested first: the plans are on
+    // the way to the first barrier
+    int32_t p_bias = 0, p_mult = 0, p_shift = 0;
+    constexpr int NTH = (1 << BITS) - 1;  // staircase thresholds per channel (4 and 2 bits)
+    int32_t p_tau[STAIR ? NTH : 1];
+    if (wv == 0 && live) {
+        if (a.bias)
+            p_bias = a.bias[ch];
+        if (a.epi == EPI_REQUANT) {
+            p_mult = a.mult[ch];
+            p_shift = a.shift[ch];
+        }
+        if constexpr (STAIR) {
+#pragma unroll
+            for (int k = 0; k < NTH; ++k)
+                p_tau[k] = a.thresh[(size_t)ch * NTH + k];
+        }
+    }
+    // ---- the first image group's bytes ----
     uint4 pf[UPF];
     auto issue = [&](int grp) {
         if constexpr (BAND) {
@@ -440,23 +499,25 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     int grp = blockIdx.x;
     if (grp < a.ngroups)
         issue(grp);
-    // the channel parameters of the plans (wave 0: bias, multiplier and
-    // shift, or the staircase thresholds), loaded now so that their latency
-    // overlaps the image and filter loads
-    int32_t p_bias = 0, p_mult = 0, p_shift = 0;
-    constexpr int NTH = (1 << BITS) - 1;  // staircase thresholds per channel (4 and 2 bits)
-    int32_t p_tau[STAIR ? NTH : 1];
-    if (wv == 0 && live) {
-        if (a.bias)
-            p_bias = a.bias[ch];
-        if (a.epi == EPI_REQUANT) {
-            p_mult = a.mult[ch];
-            p_shift = a.shift[ch];
-        }
-        if constexpr (STAIR) {
+    // ---- wide-pixel filters: the group's 32 filter rows are contiguous;
+    // the threads that stage them (waves 1-3 when wave 0 computes the plans)
+    // load them as 16-byte quads right after the image bytes, before any
+    // other work ----
+    constexpr bool early_plans = BITS != 8 || G::CHUNK;
+    constexpr int QPR = WROW / 16;                                   // quads per filter row
+    constexpr int FT = early_plans ? NT - 64 : NT;                   // staging threads
+    constexpr int FQ = G::CHUNK ? (32 * QPR + FT - 1) / FT : 1;      // quads per staging thread
+    const int ft = early_plans ? tid - 64 : tid;
+    uint4 fq[FQ];
+    if constexpr (G::CHUNK) {
+        const int nq = min(32, a.m - gy * 32) * QPR;
+        const uint8_t *wg = a.w + (size_t)gy * 32 * WROW;
 #pragma unroll
-            for (int k = 0; k < NTH; ++k)
-                p_tau[k] = a.thresh[(size_t)ch * NTH + k];
+        for (int i = 0; i < FQ; ++i) {
+            const int q = ft + i * FT;
+            fq[i] = make_uint4(0, 0, 0, 0);
+            if (ft >= 0 && q < nq)
+                fq[i] = *(const uint4 *)(wg + (size_t)q * 16);
         }
     }
 
@@ -465,9 +526,10 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     // LDS behind the image tiles: the unpacked filter units (CHUNK), then the
     // group's compression plans and fast-path votes
     uint8_t *sF = smem + (size_t)a.ipw * a.tile_bytes;
-    // the requantization plans (e0 of the 32 channels, then their e1: lanes
-    // read consecutive 16-byte entries), or [16][32 channels] staircase
-    // thresholds on the kernel's accumulator scale
+    // the requantization plans (e0 of the 32 channels, then their e1, then
+    // their three-instruction forms: lanes read consecutive 16-byte
+    // entries), or [16][32 channels] staircase thresholds on the kernel's
+    // accumulator scale
     int4 *sPlan = (int4 *)(sF + G::FLDS);
     int *sVote = (int *)(sPlan + 128);
     uint8_t *sOut = (uint8_t *)(sPlan + 129) + wv * 64 * G::OPS;  // this wave's output staging
@@ -485,9 +547,11 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             ((uint4 *)smem)[i] = f4;
     }
     // ---- the group's compression plans (requant_plan) and the wave-uniform
-    // fast paths: every channel in the 32-bit strict form; in the 32- or
-    // 64-bit strict form; every channel's code non-decreasing in the
-    // accumulator (positive multiplier).  Computed by wave 0 (whose lanes hold
+    // fast paths: every channel in the 32-bit strict form with its clamp
+    // interval in the signed 24-bit range (three instructions per code,
+    // img_plan3); in the 32-bit strict form; in the 32- or 64-bit strict
+    // form; every channel's code non-decreasing in the accumulator (positive
+    // multiplier).  Computed by wave 0 (whose lanes hold
     // the same 32 channels as every wave's) and shared through LDS (read
     // after the first staging barrier).  Sub-byte plans need no filter sums
     // and 8-bit ones of 16-byte filter units read theirs from the filter
@@ -549,41 +613,36 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 b += 128 * (int64_t)wsum;
             const int sh = p_shift < 0 ? 0 : (p_shift > 62 ? 62 : p_shift);
             requant_plan(b, p_mult, sh, a.clip_lo, a.clip_hi, a.epi == EPI_REQUANT, SL, q0, q1);
-            const bool v3 = __all(!live || q1.z == 3);
+            int4 p3;
+            const bool ok3 = img_plan3(q0, q1, p3);
+            const bool v3 = __all(!live || ok3);
+            const bool v3s = __all(!live || q1.z == 3);
             const bool v34 = __all(!live || q1.z == 3 || q1.z == 4);
             const bool vm = __all(!live || q1.z != 0 || q0.z > 0);
             if (h == 0) {
                 sPlan[r32] = q0;
                 sPlan[32 + r32] = q1;
+                sPlan[64 + r32] = p3;
             }
             if (lane == 0)
-                *sVote = (v3 ? 1 : 0) | (v34 ? 2 : 0) | (vm ? 4 : 0);
+                *sVote = (v3 ? 1 : 0) | (v34 ? 2 : 0) | (vm ? 4 : 0) | (v3s ? 16 : 0);
         }
     };
-    constexpr bool early_plans = BITS != 8 || G::CHUNK;
     if (early_plans && wv == 0)
         compute_plans();
     if constexpr (G::CHUNK) {
         // the fragment of K step s (tap s / CPT, chunk s % CPT) for lane half
         // h is packed bytes [(2 s + h) * WB, + WB) of the channel's row: unit
-        // 2 s + h.  The group's 32 rows are contiguous: the workgroup loads
-        // them as 16-byte quads, expands every unit to 16 int8 values and
-        // stores unit u of channel c at u * FP + 16 c (units of missing
-        // channels are zero)
-        constexpr int WB = G::WB, FP = G::FP, QPR = WROW / 16, UPQ = 16 / WB;
-        const int nq = min(32, a.m - gy * 32) * QPR;
-        const uint8_t *wg = a.w + (size_t)gy * 32 * WROW;
-        // staged by the threads of waves 1-3 when wave 0 computes the plans
-        constexpr int FT = early_plans ? NT - 64 : NT;
-        const int ft = early_plans ? tid - 64 : tid;
+        // 2 s + h.  Every unit of the loaded quads is expanded to 16 int8
+        // values and unit u of channel c stored at u * FP + 16 c (units of
+        // missing channels are zero)
+        constexpr int WB = G::WB, FP = G::FP, UPQ = 16 / WB;
 #pragma unroll
-        for (int i = 0; i < (32 * QPR + FT - 1) / FT; ++i) {
+        for (int i = 0; i < FQ; ++i) {
             const int q = ft + i * FT;
             if (ft < 0 || (32 * QPR % FT != 0 && q >= 32 * QPR))
                 break;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (q < nq)
-                v = *(const uint4 *)(wg + (size_t)q * 16);
+            const uint4 v = fq[i];
             const int c = q / QPR;
             uint8_t *dst = sF + (q - c * QPR) * UPQ * FP + c * 16;
             if (BITS == 8) {
@@ -717,7 +776,8 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
         __syncthreads();
         const int4 e0 = sPlan[r32], e1 = sPlan[32 + r32];
         const int votes = *sVote;
-        const bool all3 = (votes & 1) != 0, all34 = (votes & 2) != 0, mono = (votes & 4) != 0;
+        const bool all3 = (votes & 1) != 0, all34 = (votes & 2) != 0, mono = (votes & 4) != 0,
+                   all3s = (votes & 16) != 0;
         const int64_t bt = (int64_t)(((uint64_t)(uint32_t)e0.y << 32) | (uint32_t)e0.x);  // raw: bias (+ 128 wsum)
         if (grp + (int)gridDim.x < a.ngroups)
             issue(grp + gridDim.x);
@@ -842,13 +902,25 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 else
                     stair_pool(ImgConst<0>());
             } else if (all3) {
+                const int4 p3 = sPlan[64 + r32];
                 run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint32_t code[8];
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
                         int32_t x0, x1, y0, y1;
                         win(k, c0, c1, x0, x1, y0, y1);
-                        code[k] = img_code3(max(max(x0, x1), max(y0, y1)), e0, e1);
+                        code[k] = img_code3(max(max(x0, x1), max(y0, y1)), p3, e1.x);
+                    }
+                    store_pool(img, orow, hx, code);
+                });
+            } else if (all3s) {
+                run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
+                    uint32_t code[8];
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        int32_t x0, x1, y0, y1;
+                        win(k, c0, c1, x0, x1, y0, y1);
+                        code[k] = img_code3s(max(max(x0, x1), max(y0, y1)), e0, e1);
                     }
                     store_pool(img, orow, hx, code);
                 });
@@ -982,13 +1054,15 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                     stair_tiles(ImgConst<1>());
                 else
                     stair_tiles(ImgConst<0>());
-            } else if (all3) {
+            } else if (all3s) {
+                // (not the three-instruction form: its inline-asm clamp would
+                // be the first reader of the matrix results)
                 run([&](int img, int orow, int hx, const v16i &c0, const v16i &c1) {
                     uint32_t code[32];
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
-                        code[v] = img_code3(c0[v], e0, e1);
-                        code[16 + v] = img_code3(c1[v], e0, e1);
+                        code[v] = img_code3s(c0[v], e0, e1);
+                        code[16 + v] = img_code3s(c1[v], e0, e1);
                     }
                     store_tiles(img, orow, hx, code);
                 });

@@ -432,7 +432,9 @@ bool plan_img(ImgArgs &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g
     pbytes = (int)pb;
     const int64_t npix = (int64_t)x->h * x->w;
     const int64_t img_bytes = npix * pb;
-    const int sb = u == 4 ? 8 : (int)u;       // tile slot bytes (8-bit one-word pixels: a pair)
+    // tile slot bytes (8-bit one-word pixels: a pair; wide pixels: padded by
+    // 16 bytes, an odd number of 16-byte units, against bank conflicts)
+    const int sb = u == 4 ? 8 : (u >= 32 ? (int)u + 16 : (int)u);
     const int pp = wop + g->kw - 1;           // tile pitch, slots
     const int rt = 32 / wop;                  // image rows per MFMA row tile
     if (img_bytes > 8192) {
