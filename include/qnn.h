@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define QNN_ABI_VERSION 7
+#define QNN_ABI_VERSION 8
 
 typedef enum {
     QNN_OK = 0,
@@ -152,8 +152,9 @@ typedef struct {
 /* Library ABI version (QNN_ABI_VERSION). */
 int32_t qnn_abi_version(void);
 
-/* Static description of a status code; never NULL. */
-const char *qnn_status_string(qnn_status s);
+/* Static description of a status code (a qnn_status value; any other value
+ * gives "unknown status"); never NULL. */
+const char *qnn_status_string(int32_t status);
 
 /* Checks that the current HIP device is a gfx950 GPU.  Called implicitly by
  * every device entry point; QNN_ERR_DEVICE when no such device is current. */

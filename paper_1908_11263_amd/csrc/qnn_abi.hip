@@ -772,9 +772,11 @@ extern "C" {
 
 int32_t qnn_abi_version(void) { return QNN_ABI_VERSION; }
 
-const char *qnn_status_string(qnn_status s)
+const char *qnn_status_string(int32_t status)
 {
-    switch (s) {
+    // compared as an integer: a value outside the enumeration is no
+    // qnn_status, and loading it as one would be undefined
+    switch (status) {
     case QNN_OK: return "ok";
     case QNN_ERR_NULL: return "a required pointer is NULL";
     case QNN_ERR_BITS: return "unsupported or mismatched bit-width";

@@ -14,7 +14,9 @@ import os
 import re
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libqnn.so")
+# QNN_LIBRARY names another build of the same sources (the sanitizer test
+# loads a host-instrumented build)
+LIB_PATH = os.environ.get("QNN_LIBRARY") or os.path.join(HERE, "libqnn.so")
 HEADER = os.path.join(os.path.dirname(HERE), "include", "qnn.h")
 
 EPI_REQUANT, EPI_THRESH1, EPI_RAW32, EPI_STAIR = 0, 1, 2, 3

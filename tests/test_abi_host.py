@@ -25,7 +25,7 @@ def test_exports_every_header_function(q, L):
     assert len(names) >= 12
     for name in names:
         assert hasattr(L, name), name
-    assert L.qnn_abi_version() == 7
+    assert L.qnn_abi_version() == 8
 
 
 def test_exports_every_calibration_function(q, L):
