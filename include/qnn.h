@@ -19,6 +19,11 @@
  *   pixel occupies ceil(C*b/8) bytes ("pixel bytes"); convolution, pooling
  *   and linear inputs require pixel bytes to be a multiple of 4 (pad C with
  *   zero channels and zero weights, which leaves every result unchanged).
+ *   One exception: a convolution also takes 2-byte pixels of 4 channels at
+ *   4 bits (a network's first layer: 3 image channels and a zero channel)
+ *   when the whole-image kernel covers it (see QNN_TILE_IMAGE: stride 1,
+ *   3x3 or 5x5 filters, output rows of at most 32 pixels), else
+ *   QNN_ERR_ALIGN.
  * Values.  Activations are unsigned codes (0 .. 2^b - 1) for b = 8, 4, 2;
  *   weights are two's complement codes (-2^(b-1) .. 2^(b-1) - 1).  At b = 1
  *   both operands hold +1 (bit 1) or -1 (bit 0) (Sec. III-A, Eq. (5)).
@@ -129,7 +134,8 @@ typedef struct {
  * most 32 pixels, images of at most 8 KB, QNN_EPI_REQUANT (also fused with
  * max-pooling) or QNN_EPI_RAW32, M*bits a multiple of 32, and input pixels
  * of 4 packed bytes (a network's first layer: e.g. 3 image channels padded
- * to 4 at 8 bits) or of 16 / 32 packed bytes (32 channels at 4 / 8 bits, 64
+ * to 4 at 8 bits), of 2 packed bytes (4 channels at 4 bits), or of 16 / 32
+ * packed bytes (32 channels at 4 / 8 bits, 64
  * at 2 / 4 bits) with at most 28 K steps of 32 (5x5 filters: 32 channels at
  * 8 or 4 bits).  The library picks it by itself for every layer that
  * qualifies; tile_m = tile_n = waves = 0.  A layer that does not qualify

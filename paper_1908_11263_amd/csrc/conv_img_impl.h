@@ -81,6 +81,18 @@ struct BandTaps {
     }
 };
 
+// Half-word pixels (4 channels at 4 bits, codes n0..n3): activations as the
+// bytes n0, n2, n1, n3 and weights as 16 times the same order, the K order
+// of the 4-bit packed words (stage_word<4>, w4_word) within one 16-bit pixel.
+__device__ __forceinline__ uint32_t stage_half4(uint32_t v)
+{
+    return (v & 0x0F0Fu) | (((v >> 4) & 0x0F0Fu) << 16);
+}
+__device__ __forceinline__ uint32_t w4_half(uint32_t v)
+{
+    return ((v << 4) & 0xF0F0u) | ((v & 0xF0F0u) << 16);
+}
+
 // Geometry of one instance: BITS-bit codes, pixels of P packed bytes.
 template <int BITS, int P, int KH, int KW, int WOP>
 struct ImgGeom {
@@ -411,6 +423,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
     static_assert(!STAIR || BITS != 8, "the staircase epilogue is built at 4 and 2 bits");
     typedef ImgGeom<BITS, P, KH, KW, WOP> G;
     static_assert(!BAND || P >= 16, "row bands are built for pixels of whole 16-byte quads");
+    static_assert(P != 2 || BITS == 4, "half-word pixels are built at 4 bits (4 channels)");
     constexpr int NW = 4, NT = 256;
     constexpr int SB = G::SB, PP = G::PP, RB = G::RB, RT = G::RT, DY = G::DY, KS = G::KS;
     constexpr int SL = BITS == 4 ? 4 : (BITS == 2 ? 6 : 0);  // log2 of the weight scale
@@ -482,7 +495,7 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             if (a.quads) {
                 if (q < ni * imgq)
                     pf[u] = *(const uint4 *)(src + (size_t)q * 16);
-            } else {
+            } else if constexpr (P == 4) {
                 // one-word pixels, npix not a multiple of 4 (a single image per step)
                 const uint32_t *s4 = (const uint32_t *)src;
                 if (4 * q < npix)
@@ -493,6 +506,15 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                     pf[u].z = s4[4 * q + 2];
                 if (4 * q + 3 < npix)
                     pf[u].w = s4[4 * q + 3];
+            } else {
+                // half-word pixels, npix not a multiple of 8 (a single image per step)
+                const uint16_t *s2 = (const uint16_t *)src;
+                uint32_t d[4] = {0, 0, 0, 0};
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (8 * q + j < npix)
+                        d[j >> 1] |= (uint32_t)s2[8 * q + j] << (16 * (j & 1));
+                pf[u] = make_uint4(d[0], d[1], d[2], d[3]);
             }
         }
     };
@@ -671,9 +693,12 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 const int ky = (tp >> 8) + h * DY, kx = tp & 255;
                 uint32_t v = 0;
                 if (tp >= 0 && live && ky < KH)
-                    v = *(const uint32_t *)(wb + (ky * KW + kx) * 4);
+                    v = P == 2 ? (uint32_t)*(const uint16_t *)(wb + (ky * KW + kx) * 2)
+                               : *(const uint32_t *)(wb + (ky * KW + kx) * 4);
                 if (BITS == 8) {
                     d[t] = v;
+                } else if (P == 2) {
+                    d[t] = w4_half(v);
                 } else if (BITS == 4) {
                     const uint2 e = w4_word(v);
                     d[2 * t] = e.x;
@@ -722,23 +747,32 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
 #pragma unroll
         for (int u = 0; u < UPF; ++u) {
             const int q = tid + u * NT;
-            if (P == 4) {
-                // four one-word pixels per quad (one image per step when the
-                // image is not a whole number of quads)
+            if (P <= 4) {
+                // 16 / P one-word (or half-word) pixels per quad (one image
+                // per step when the image is not a whole number of quads)
+                constexpr int PPQ = 16 / P;
                 const int ii = a.quads ? (int)fdiv((uint32_t)q, a.div_imgq) : 0;
-                const int p0 = 4 * (q - ii * imgq);
+                const int p0 = PPQ * (q - ii * imgq);
                 if (ii < ni && p0 < npix) {
                     uint8_t *tile = smem + ii * a.tile_bytes;
                     int iy = (int)fdiv((uint32_t)p0, a.div_w);
                     int ix = p0 - iy * a.w_;
                     const uint32_t wd[4] = {pf[u].x, pf[u].y, pf[u].z, pf[u].w};
 #pragma unroll
-                    for (int j = 0; j < 4; ++j) {
+                    for (int j = 0; j < PPQ; ++j) {
                         if (p0 + j < npix) {
                             uint8_t *dst = tile + ((iy + a.ph) * PP + ix + a.pw) * SB;
-                            stage_word<BITS>(dst, wd[j]);
-                            if (BITS == 8 && ix + a.pw > 0)
-                                stage_word<BITS>(dst - 4, wd[j]);  // second pixel of the slot on its left
+                            if constexpr (P == 2) {
+                                // one unpacked word per pixel, pixel pairs per slot as at 8 bits
+                                const uint32_t e = stage_half4(wd[j >> 1] >> (16 * (j & 1)));
+                                *(uint32_t *)dst = e;
+                                if (ix + a.pw > 0)
+                                    *(uint32_t *)(dst - 4) = e;
+                            } else {
+                                stage_word<BITS>(dst, wd[j]);
+                                if (BITS == 8 && ix + a.pw > 0)
+                                    stage_word<BITS>(dst - 4, wd[j]);  // second pixel of the slot on its left
+                            }
                         }
                         if (++ix == a.w_) {
                             ix = 0;

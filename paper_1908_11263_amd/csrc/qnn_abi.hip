@@ -416,7 +416,7 @@ bool plan_img(ImgArgs &p, const qnn_tensor *x, int32_t m, const qnn_conv_geom *g
         return false;
     const int64_t u = pb * 8 / bits;  // unpacked bytes per pixel
     const int taps = g->kh * g->kw;
-    if (pb == 4) {
+    if (pb == 4 || (pb == 2 && bits == 4)) {
         wop = 32;
     } else if (pb == 16 || pb == 32) {
         if (u < 32 || taps * (u / 32) > 28)
@@ -549,7 +549,10 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     if (y->bits != obits)
         return QNN_ERR_BITS;
     const int64_t pb = pixel_bytes64(x);
-    if ((int64_t)x->c * x->bits % 32 != 0)
+    // whole 4-byte pixels; or half-word pixels (4 channels at 4 bits), which
+    // only the whole-image kernel reads (checked where it is chosen)
+    const bool half_word = (int64_t)x->c * x->bits == 16 && x->bits == 4;
+    if ((int64_t)x->c * x->bits % 32 != 0 && !half_word)
         return QNN_ERR_ALIGN;
     const int64_t K = (int64_t)g->kh * g->kw * x->c;
     if (K > max_k_for(x->bits))
@@ -624,7 +627,9 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
             p.y = (uint8_t *)y_dev;
             p.ypb = ypb;
             hipError_t err;
-            if (pbytes == 4)
+            if (pbytes == 2)
+                err = launch_conv_img_p2(p, x->bits, g->kh, cus, s);
+            else if (pbytes == 4)
                 err = launch_conv_img_p4(p, x->bits, g->kh, cus, s);
             else if (pbytes == 16)
                 err = launch_conv_img_p16(p, x->bits, g->kh, wop, cus, s);
@@ -633,8 +638,10 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
             return err == hipSuccess ? QNN_OK : QNN_ERR_LAUNCH;
         }
         if (force_img)
-            return QNN_ERR_UNSUPPORTED;
+            return half_word ? QNN_ERR_ALIGN : QNN_ERR_UNSUPPORTED;
     }
+    if (half_word)
+        return QNN_ERR_ALIGN;
 
     // a filter covering the whole image with raw outputs (the network's
     // classifier): the fully connected kernel, unless the caller forces a tile

@@ -145,6 +145,7 @@ hipError_t launch_conv_xnor(const XnorArgs &a, hipStream_t s);
 // whole-image kernel; hipErrorInvalidValue for a shape with no built
 // instance; the grid fills the cus compute units with resident workgroups
 hipError_t launch_conv_img_p4(const ImgArgs &a, int bits, int k, int cus, hipStream_t s);
+hipError_t launch_conv_img_p2(const ImgArgs &a, int bits, int k, int cus, hipStream_t s);
 hipError_t launch_conv_img_p16(const ImgArgs &a, int bits, int k, int wop, int cus, hipStream_t s);
 hipError_t launch_conv_img_p32(const ImgArgs &a, int bits, int k, int wop, int cus, hipStream_t s);
 // fully connected layer with raw outputs: K a multiple of 64 (linear.hip)

@@ -239,13 +239,13 @@ def cifar_network(bits=8, n=4096, seed=4):
     """Three 5x5 conv layers (3->32, 32->32, 32->64, pad 2, requant + ReLU clip,
     2x2 max-pool after each) and a 1024->10 classifier with int32 logits.
 
-    The 3 image channels are padded with zero channels (and zero weights) to a
-    pixel of 4 bytes: 4 channels at 8 bits, 8 channels at 4 bits."""
+    The 3 image channels are padded with a zero channel (and zero weights) to
+    4 channels: a pixel of 4 bytes at 8 bits, of 2 bytes at 4 bits."""
     rng = np.random.default_rng(seed)
     if bits == 8:
         xr, wr, br, shift, clip, cpad = (0, 255), (-128, 127), (-4096, 4096), 25, (0, 255), 4
     elif bits == 4:
-        xr, wr, br, shift, clip, cpad = (0, 15), (-7, 7), (-256, 256), 21, (0, 15), 8
+        xr, wr, br, shift, clip, cpad = (0, 15), (-7, 7), (-256, 256), 21, (0, 15), 4
     else:
         raise ValueError("CIFAR-shaped network is defined at 8 and 4 bits")
     x3 = _draw(rng, xr[0], xr[1], (n, 32, 32, 3))

@@ -129,6 +129,28 @@ def test_conv_validation_on_host(q, L, case, status):
     assert call_conv(q, L, **args) == status
 
 
+REQ4 = (0, None, FAKE, FAKE, None, 0, 15)
+
+
+@pytest.mark.parametrize("g,xs,ys", [
+    ((3, 3, 2, 2, 1, 1), (1, 8, 8, 4), (1, 4, 4, 32, 4)),     # stride 2: not the whole-image kernel
+    ((1, 1, 1, 1, 0, 0), (1, 8, 8, 4), (1, 8, 8, 32, 4)),     # 1x1 filter
+    ((3, 3, 1, 1, 1, 1), (1, 8, 40, 4), (1, 8, 40, 32, 4)),   # rows of 40 outputs
+])
+def test_half_word_pixels_outside_the_image_kernel(q, L, g, xs, ys):
+    """2-byte pixels (4 channels at 4 bits) are read by the whole-image kernel
+    only; other layers are refused on the host with QNN_ERR_ALIGN."""
+    assert call_conv(q, L, xs, 4, 32, g, REQ4, ys) == 5
+
+
+def test_half_word_pixels_at_other_widths(q, L):
+    """2-byte pixels at 8 bits (2 channels) or 2 bits (8 channels) are not
+    built: QNN_ERR_ALIGN."""
+    assert call_conv(q, L, (1, 8, 8, 2), 8, 32, (3, 3, 1, 1, 1, 1), REQ8, (1, 8, 8, 32, 8)) == 5
+    assert call_conv(q, L, (1, 8, 8, 8), 2, 32, (3, 3, 1, 1, 1, 1), (0, None, FAKE, FAKE, None, 0, 3),
+                     (1, 8, 8, 32, 2)) == 5
+
+
 def test_int1_requires_threshold_or_raw(q, L):
     assert call_conv(q, L, (1, 4, 4, 32), 1, 8, (3, 3, 1, 1, 1, 1), (0, None, FAKE, FAKE, None, 0, 1),
                      (1, 4, 4, 8, 1)) == 2

@@ -101,6 +101,27 @@ def test_img_requant(qnn, orc, bits, pool):
             check(qnn, orc, L, tile=IMAGE)
 
 
+@pytest.mark.parametrize("pool", [False, True])
+def test_img_half_word_pixels(qnn, orc, pool):
+    """2-byte pixels (4 channels at 4 bits: a network's first layer with 3
+    image channels and a zero channel): requantized, pooled, raw sums and the
+    staircase, over the first-layer shapes (ragged sizes load the image
+    half-word by half-word)."""
+    for i, (n, h, w, m, k, pad) in enumerate(SHAPES):
+        L = layer(4, n, h, w, m, k, pad, seed=300 + i, c=4)
+        if pool and (L.ho < 2 or L.wo < 2):
+            continue
+        check(qnn, orc, L, pool=pool)
+        if not pool:
+            check(qnn, orc, L, epi="raw32")
+            check(qnn, orc, L, tile=IMAGE)
+    for i, (n, h, w, m, k, pad) in enumerate(SHAPES[:4]):
+        S = stair_img_layer(4, 4, n, h, w, m, k, pad, seed=310 + i, sorted_=i % 2 == 0)
+        if pool and (S.ho < 2 or S.wo < 2):
+            continue
+        check(qnn, orc, S, pool=pool)
+
+
 @pytest.mark.parametrize("bits", [8, 4, 2])
 def test_img_raw32(qnn, orc, bits):
     for i, (n, h, w, m, k, pad) in enumerate(SHAPES):
