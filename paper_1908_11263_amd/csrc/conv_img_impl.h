@@ -190,6 +190,56 @@ __device__ __forceinline__ void img_steps(const uint8_t *p0, const uint8_t *p1, 
     }
 }
 
+// The same K steps with the im2col fragments read D steps ahead of their
+// MFMAs: a ring of D + 1 fragment pairs, the order held by scheduling
+// barriers (left to itself the compiler reads each pair right before its
+// MFMAs and waits out the local-memory latency at every step).  Used for
+// row bands, whose 18 K steps per tile pair make that latency a chain
+// (INT-4 batch-64 layer 6.93 -> 6.65 us, measured side by side); the shorter K loops
+// of whole small images gain nothing from it.
+template <int BITS, int P, int KH, int KW, int WOP, int S, int D>
+__device__ __forceinline__ void img_pipe(const uint8_t *p0, const uint8_t *p1, const v4i *A, v16i &acc0,
+                                         v16i &acc1, v4i *b0, v4i *b1)
+{
+    constexpr int KS = ImgGeom<BITS, P, KH, KW, WOP>::KS;
+    if constexpr (S < KS) {
+        if constexpr (S + D < KS) {
+            b0[(S + D) % (D + 1)] = img_frag<BITS, P, KH, KW, WOP, S + D>(p0);
+            b1[(S + D) % (D + 1)] = img_frag<BITS, P, KH, KW, WOP, S + D>(p1);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        constexpr int k = S % (D + 1);
+        if constexpr (S == 0) {
+            acc0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b0[k], A[S], (v16i){}, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b1[k], A[S], (v16i){}, 0, 0, 0);
+        } else {
+            acc0 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b0[k], A[S], acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_i32_32x32x32_i8(b1[k], A[S], acc1, 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        img_pipe<BITS, P, KH, KW, WOP, S + 1, D>(p0, p1, A, acc0, acc1, b0, b1);
+    }
+}
+
+template <int BITS, int P, int KH, int KW, int WOP, int S, int D>
+__device__ __forceinline__ void img_pipe_fill(const uint8_t *p0, const uint8_t *p1, v4i *b0, v4i *b1)
+{
+    if constexpr (S < D && S < ImgGeom<BITS, P, KH, KW, WOP>::KS) {
+        b0[S] = img_frag<BITS, P, KH, KW, WOP, S>(p0);
+        b1[S] = img_frag<BITS, P, KH, KW, WOP, S>(p1);
+        img_pipe_fill<BITS, P, KH, KW, WOP, S + 1, D>(p0, p1, b0, b1);
+    }
+}
+
+template <int BITS, int P, int KH, int KW, int WOP, int D>
+__device__ __forceinline__ void img_steps_ahead(const uint8_t *p0, const uint8_t *p1, const v4i *A, v16i &acc0,
+                                                v16i &acc1)
+{
+    v4i b0[D + 1], b1[D + 1];
+    img_pipe_fill<BITS, P, KH, KW, WOP, 0, D>(p0, p1, b0, b1);
+    img_pipe<BITS, P, KH, KW, WOP, 0, D>(p0, p1, A, acc0, acc1, b0, b1);
+}
+
 // Scale-and-clamp code of one (scaled) accumulator from the channel's plan
 // (requant_plan): any mode.
 template <int SL>
@@ -826,7 +876,10 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                 const int tp = it - ii * a.pairs;
                 const uint8_t *p0 = smem + ii * a.tile_bytes + 2 * tp * RT * RB + lane_slot;
                 v16i c0, c1;
-                img_steps<BITS, P, KH, KW, WOP, 0>(p0, p0 + RT * RB, A, c0, c1);
+                if constexpr (BAND)
+                    img_steps_ahead<BITS, P, KH, KW, WOP, 4>(p0, p0 + RT * RB, A, c0, c1);
+                else
+                    img_steps<BITS, P, KH, KW, WOP, 0>(p0, p0 + RT * RB, A, c0, c1);
                 // an opaque copy of the lane half keeps the general paths'
                 // per-register pixel indexes and bounds checks in this body
                 // (hoisted out of the loop they would hold a register or a
@@ -878,8 +931,18 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                                       ((size_t)((orow >> 1) + lane / WP) * WP + lane % WP) * YP;
                         if constexpr (YG >= 16) {
 #pragma unroll
-                            for (int i = 0; i < YG; i += 16)
-                                *(uint4 *)(yt + i) = *(const uint4 *)(sOut + lane * YG + i);
+                            for (int i = 0; i < YG; i += 16) {
+                                // a first layer's output (its largest
+                                // stream, twice its input at 8 bits) is
+                                // written past the caches (INT-8 / INT-4
+                                // CIFAR first layer 30.8 -> 29.4 / 28.3 ->
+                                // 27.2 us, measured side by side; no gain on the
+                                // later layers)
+                                if constexpr (P <= 4)
+                                    __builtin_nontemporal_store(*(const v4i *)(sOut + lane * YG + i), (v4i *)(yt + i));
+                                else
+                                    *(uint4 *)(yt + i) = *(const uint4 *)(sOut + lane * YG + i);
+                            }
                         } else {
                             *(uint2 *)yt = *(const uint2 *)(sOut + lane * YG);
                         }
