@@ -568,7 +568,12 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
             }
         }
     };
+    // row bands: the workgroups of one XCD (dispatched round-robin over the
+    // eight, workgroup i on XCD i mod 8) take consecutive bands, so the halo
+    // rows two bands of an image share are fetched into one L2
     int grp = blockIdx.x;
+    if (BAND && gridDim.x % 8 == 0)
+        grp = (int)(blockIdx.x % 8) * (int)(gridDim.x / 8) + (int)(blockIdx.x / 8);
     if (grp < a.ngroups)
         issue(grp);
     // ---- wide-pixel filters: the group's 32 filter rows are contiguous;
