@@ -195,8 +195,8 @@ __device__ __forceinline__ void img_steps(const uint8_t *p0, const uint8_t *p1, 
 // barriers (left to itself the compiler reads each pair right before its
 // MFMAs and waits out the local-memory latency at every step).  Used for
 // row bands, whose 18 K steps per tile pair make that latency a chain
-// (INT-4 batch-64 layer 6.93 -> 6.65 us, measured side by side); the shorter K loops
-// of whole small images gain nothing from it.
+// (INT-4 batch-64 layer 6.93 -> 6.65 us, measured side by side); the
+// shorter K loops of whole small images gain nothing from it.
 template <int BITS, int P, int KH, int KW, int WOP, int S, int D>
 __device__ __forceinline__ void img_pipe(const uint8_t *p0, const uint8_t *p1, const v4i *A, v16i &acc0,
                                          v16i &acc1, v4i *b0, v4i *b1)
@@ -569,8 +569,9 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
         }
     };
     // row bands: the workgroups of one XCD (dispatched round-robin over the
-    // eight, workgroup i on XCD i mod 8) take consecutive bands, so the halo
-    // rows two bands of an image share are fetched into one L2
+    // eight, workgroup i on XCD i mod 8; with gridDim.x a multiple of 8 both
+    // channel groups of a band land on the same XCD) take consecutive bands,
+    // so the halo rows two bands of an image share are fetched into one L2
     int grp = blockIdx.x;
     if (BAND && gridDim.x % 8 == 0)
         grp = (int)(blockIdx.x % 8) * (int)(gridDim.x / 8) + (int)(blockIdx.x / 8);
@@ -941,8 +942,8 @@ __global__ void __launch_bounds__(256) conv_img_kernel(ImgArgs a)
                                 // stream, twice its input at 8 bits) is
                                 // written past the caches (INT-8 / INT-4
                                 // CIFAR first layer 30.8 -> 29.4 / 28.3 ->
-                                // 27.2 us, measured side by side; no gain on the
-                                // later layers)
+                                // 27.2 us, measured side by side; no gain
+                                // on the later layers)
                                 if constexpr (P <= 4)
                                     __builtin_nontemporal_store(*(const v4i *)(sOut + lane * YG + i), (v4i *)(yt + i));
                                 else
