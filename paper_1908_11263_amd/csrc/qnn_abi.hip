@@ -338,6 +338,29 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
         return QNN_OK;
     }
     static const int cand[5][2] = {{4, 1}, {2, 2}, {2, 1}, {1, 2}, {1, 1}};
+    // the e2m1 path: eight-wave tiles first, whenever one fits the local
+    // memory with at most one tile per compute unit.  Its staged filter rows
+    // are 2x / 4x the packed ones (INT-2 / INT-1), so sharing them between
+    // twice the pixels pays most here (INT-1 batch-1024 layer: 2x1 eight-wave
+    // tiles 33.6 us against 51.0 us for the 1x1 four-wave tile the general
+    // rule below picks)
+    if (f4 && allow_nw8 && !a.pool && a.epi != EPI_STAIR && al16) {
+        for (int i = 1; i < 5; ++i) {
+            const int cwm = cand[i][0], cwn = cand[i][1];
+            const int MT = 32 * cwm;
+            if ((MT > 32 && MT - 32 >= b.m) || MT > ((b.m + 31) / 32) * 32)
+                continue;
+            ConvArgs c8 = b;
+            const int64_t lds8 = fit_tile(c8, MT, 256 * cwn, bits, obits, (int64_t)MT * b.kp, tab_bytes, true);
+            if (lds8 < 0 || lds8 > kLdsBytes || c8.ntiles > kPlanCus)
+                continue;
+            a = c8;
+            wm = cwm;
+            wn = cwn;
+            nw = 8;
+            return QNN_OK;
+        }
+    }
     // pass 2 (pooled layers and the e2m1 path, which have no other kernel to
     // fall back on): any tile that fits, even with few tiles
     const bool last_resort = a.pool || f4;
