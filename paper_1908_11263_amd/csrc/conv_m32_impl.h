@@ -868,6 +868,12 @@ hipError_t launch_conv_m32_bits(const ConvArgs &a, int wm, int wn, int al16, int
     // eight-wave workgroups: plain instances for layers with one tile per workgroup
     QNN_CASE32_X(1, 1, 1, false, 8) QNN_CASE32_X(2, 1, 1, false, 8)
     QNN_CASE32_X(1, 2, 1, false, 8) QNN_CASE32_X(2, 2, 1, false, 8)
+    if constexpr (F4) {
+        // the e2m1 path also walks several tiles per eight-wave workgroup
+        // (one workgroup per compute unit keeps its staged filter rows)
+        QNN_CASE32_X(1, 1, 1, true, 8) QNN_CASE32_X(2, 1, 1, true, 8)
+        QNN_CASE32_X(1, 2, 1, true, 8) QNN_CASE32_X(2, 2, 1, true, 8)
+    }
     if constexpr (BITS == 8 && !F4) {
         // 128-channel wave tiles: 8-bit only (the sub-byte expansion does not fit
         // two workgroups' register budget at this width)

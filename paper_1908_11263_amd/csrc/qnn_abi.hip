@@ -339,11 +339,12 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
     }
     static const int cand[5][2] = {{4, 1}, {2, 2}, {2, 1}, {1, 2}, {1, 1}};
     // the e2m1 path: eight-wave tiles first, whenever one fits the local
-    // memory with at most one tile per compute unit.  Its staged filter rows
-    // are 2x / 4x the packed ones (INT-2 / INT-1), so sharing them between
-    // twice the pixels pays most here (INT-1 batch-1024 layer: 2x1 eight-wave
-    // tiles 33.6 us against 51.0 us for the 1x1 four-wave tile the general
-    // rule below picks)
+    // memory, one workgroup per compute unit walking its channel group's
+    // tiles.  Its staged filter rows are 2x / 4x the packed ones (INT-2 /
+    // INT-1), so sharing them between more pixels pays most here (INT-1
+    // batch-1024 layer: 2x1 eight-wave tiles 33.6 us with one tile per
+    // workgroup, 25.5 us walking four, against 51.0 us for the 1x1 four-wave
+    // tile the general rule below picks)
     if (f4 && allow_nw8 && !a.pool && a.epi != EPI_STAIR && al16) {
         for (int i = 1; i < 5; ++i) {
             const int cwm = cand[i][0], cwn = cand[i][1];
@@ -352,7 +353,7 @@ qnn_status plan_conv_m32(ConvArgs &a, int bits, int &wm, int &wn, int &al16, int
                 continue;
             ConvArgs c8 = b;
             const int64_t lds8 = fit_tile(c8, MT, 256 * cwn, bits, obits, (int64_t)MT * b.kp, tab_bytes, true);
-            if (lds8 < 0 || lds8 > kLdsBytes || c8.ntiles > kPlanCus)
+            if (lds8 < 0 || lds8 > kLdsBytes)
                 continue;
             a = c8;
             wm = cwm;
@@ -734,10 +735,11 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     st = device_info(&cus);
     if (st != QNN_OK)
         return st;
-    if (use32 && nw == 8 && a.ntiles > cus) {
+    if (use32 && nw == 8 && a.ntiles > cus && !f4) {
         // an eight-wave plan needs one tile per workgroup and one workgroup
-        // per compute unit: on a device with fewer compute units the layer
-        // takes four waves
+        // per compute unit (the e2m1 path also has eight-wave instances that
+        // walk several tiles): on a device with fewer compute units the
+        // layer takes four waves
         if (force && !(f4 && force->tile_m == 0))
             return QNN_ERR_UNSUPPORTED;
         a = a0;
@@ -775,6 +777,8 @@ qnn_status run_conv(const qnn_tensor *x, const void *x_dev, int32_t m, const voi
     const int mtiles = (m + MT - 1) / MT;
     const int per_cu = (a.lds_bytes * 2 <= kLdsBytes && nw == 4) ? 2 : 1;
     int64_t gx = (int64_t)cus * per_cu;
+    if (f4 && nw == 8)
+        gx = cus / mtiles > 1 ? cus / mtiles : 1;  // one workgroup per compute unit in all
     if (gx > a.ntiles)
         gx = a.ntiles;
     if (gx < 1)
