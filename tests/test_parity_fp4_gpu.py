@@ -151,3 +151,14 @@ def test_fp4_int1_layer_batch1024(qnn, orc):
     L = synth.int1_layer()
     check(qnn, orc, L)
     check(qnn, orc, with_epi(L, "raw32"))
+
+
+def test_fp4_workgroups_walk_several_tiles(qnn, orc):
+    """The library's FP4 plan (eight-wave tiles, one workgroup per compute
+    unit walking its channel group's tiles) with more tiles than workgroups,
+    an uneven split and a ragged last tile: 301 images of 8x8x256 at 1 bit
+    (76 tiles of four images for 64 workgroups per channel group), and 520
+    images of 16x16x128 at 2 bits with 64 filters (260 tiles of two images
+    for 256 workgroups)."""
+    check(qnn, orc, int1_layer(301, 8, 8, 256, 256, 3, seed=25))
+    check(qnn, orc, layer(520, 16, 16, 128, 64, 3, seed=26))
