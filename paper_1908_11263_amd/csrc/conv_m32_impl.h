@@ -804,6 +804,30 @@ __global__ void __launch_bounds__(64 * NW, 8 / NW) conv_m32_kernel(ConvArgs a)
                         dst[idx] = pack_codes_word<BITS>(sC + p * cs + q * CPW);
                     }
                 }
+            } else if (a.oquad16 && (a.obq & 3) == 0 && obn == 4 * a.obq && (a.ypb & 15) == 0 &&
+                       (ob0 & 15) == 0) {
+                // whole 16-byte quads of a pixel's channel range (aligned):
+                // one thread per pixel of the tile, its tile coordinates
+                // computed once, 16-byte stores (INT-2 batch-256 layer
+                // 15.1 -> 14.1 us against one thread per 4-byte word)
+                const int nq = a.obq >> 2;
+                for (int p = tid; p < tile_px; p += NT) {
+                    const int tI = (int)fdiv((uint32_t)p, a.div_tile_px);
+                    const int rem = p - tI * a.th * a.tw;
+                    const int py = (int)fdiv((uint32_t)rem, a.div_tw);
+                    const int px = rem - py * a.tw;
+                    const int nn = T.n0 + tI, oy = T.oy0 + py, ox = T.ox0 + px;
+                    if (nn >= a.n || oy >= a.ho || ox >= a.wo)
+                        continue;
+                    const size_t gp = (size_t)(nn * a.ho + oy) * a.wo + ox;
+                    uint4 *dst = (uint4 *)(a.y + gp * a.ypb + ob0);
+                    for (int j = 0; j < nq; ++j) {
+                        const uint8_t *src = sC + p * cs + 4 * j * CPW;
+                        dst[j] = make_uint4(pack_codes_word<BITS>(src), pack_codes_word<BITS>(src + CPW),
+                                            pack_codes_word<BITS>(src + 2 * CPW),
+                                            pack_codes_word<BITS>(src + 3 * CPW));
+                    }
+                }
             } else {
                 const int tq4 = tile_px * a.obq;
                 for (int idx = tid; idx < tq4; idx += NT) {
