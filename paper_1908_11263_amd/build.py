@@ -26,9 +26,10 @@ FLAGS = [
 
 # per-source extra flags: the whole-image kernels keep their MFMA
 # accumulators in ordinary VGPRs (their epilogues read them right away, and
-# the accumulation registers would cost copies and occupancy)
-_VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
-EXTRA = {"conv_img_p4.hip": _VGPR_FORM, "conv_img_p16.hip": _VGPR_FORM, "conv_img_p32.hip": _VGPR_FORM}
+# the accumulation registers would cost copies and occupancy), and their
+# twelve leading scalar arguments are preloaded into scalar registers
+_IMG = ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mllvm", "-amdgpu-kernarg-preload-count=12"]
+EXTRA = {"conv_img_p4.hip": _IMG, "conv_img_p16.hip": _IMG, "conv_img_p32.hip": _IMG}
 
 
 def sources():
