@@ -29,7 +29,9 @@ FLAGS = [
 # the accumulation registers would cost copies and occupancy), and their
 # twelve leading scalar arguments are preloaded into scalar registers
 _IMG = ["-mllvm", "-amdgpu-mfma-vgpr-form", "-mllvm", "-amdgpu-kernarg-preload-count=12"]
-EXTRA = {"conv_img_p4.hip": _IMG, "conv_img_p16.hip": _IMG, "conv_img_p32.hip": _IMG}
+# the classifier kernel's eight scalar arguments likewise
+EXTRA = {"conv_img_p4.hip": _IMG, "conv_img_p16.hip": _IMG, "conv_img_p32.hip": _IMG,
+         "linear.hip": ["-mllvm", "-amdgpu-kernarg-preload-count=8"]}
 
 
 def sources():
