@@ -157,17 +157,20 @@ __device__ __forceinline__ void stage_w16(int8_t *dst, uint4 v)
 //   modes 1, 2: e0 = {a_base, D, mult, R}, e1 = {Q, shift, mode, 0}
 //   direct:     e0 = {bias lo, bias hi, mult, shift}, e1 = {0, 0, 0, 0}
 // (RAW32 uses the slow word's bias only.)
-// floor(a / b) for b > 0 and |a| < 2^52: the double quotient is within one
-// of the true one and is corrected exactly in integers.
+// floor(a / b) for 0 < b < 2^31 and |a| < 2^40: the hardware reciprocal of b
+// refined by two Newton steps times a is within one of the true quotient
+// (within 2^-10 of it: relative error below 2^-50), and the estimate is
+// corrected exactly in integers.  No division sequence: its steps share the
+// VCC register, which keeps two divisions from overlapping.
 __device__ __forceinline__ int64_t floor_div_pos(int64_t a, int64_t b)
 {
-    int64_t q = (int64_t)floor((double)a / (double)b);
-    const int64_t r = a - q * b;
-    if (r < 0)
-        q -= 1;
-    else if (r >= b)
-        q += 1;
-    return q;
+    const double bd = (double)b;
+    double r = __builtin_amdgcn_rcp(bd);
+    r = __builtin_fma(__builtin_fma(-bd, r, 1.0), r, r);
+    r = __builtin_fma(__builtin_fma(-bd, r, 1.0), r, r);
+    const int64_t q = (int64_t)__builtin_floor((double)a * r);
+    const int64_t rem = a - q * b;
+    return q + (int64_t)(rem >= b) - (int64_t)(rem < 0);
 }
 
 __device__ __forceinline__ void requant_plan(int64_t bias, int32_t mult, int32_t shift, int32_t lo,
