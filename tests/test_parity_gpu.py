@@ -187,6 +187,22 @@ def test_wide_filters(qnn, orc, bits):
     check_layer(orc, make(bits, 2, 6, 6, c, 96, 3, shift=14))
 
 
+@pytest.mark.parametrize("bits", [8, 4, 2])
+def test_plan_extremes(qnn, orc, bits):
+    """The largest shift the plans take (30) with small multipliers (threshold
+    quotients up to 2^38: the floor divisions at the top of their range) and
+    with multipliers just below 2^shift, and shift 24 with multipliers
+    around 2^21, on the general kernels (pixels of two words and more)."""
+    hi = (1 << bits) - 1
+    unit = 32 // bits
+    for j, (mult_rng, shift) in enumerate([((1, 1 << 8), 30), ((1 << 29, 1 << 30), 30),
+                                           ((1 << 20, 1 << 22), 24)]):
+        L = synth.conv_layer("plan_int%d" % bits, bits, 2, 9, 11, 2 * unit, 40, 3, 1, 60 + j, (0, hi),
+                             (-(1 << (bits - 1)), (1 << (bits - 1)) - 1), bias_rng=(-hi * 50, hi * 50),
+                             mult_rng=mult_rng, shift=shift, clip=(0, hi))
+        check_layer(orc, L)
+
+
 def test_batch_zero_launches_nothing(qnn):
     import torch
     x = torch.zeros((0, 4, 4, 4), dtype=torch.uint8, device="cuda")

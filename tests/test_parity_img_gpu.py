@@ -133,13 +133,19 @@ def test_img_raw32(qnn, orc, bits):
 @pytest.mark.parametrize("bits", [8, 4, 2])
 def test_img_plan_modes(qnn, orc, bits):
     """Multipliers above 2^shift (the general plan forms), shift 0 and clip
-    bounds inside the code range, and multipliers that are zero or negative
-    (the compression is not monotone: codes are pooled after it)."""
+    bounds inside the code range, multipliers that are zero or negative
+    (the compression is not monotone: codes are pooled after it), and the
+    largest shift the plans take (30) with small and large multipliers, whose
+    threshold quotients reach 2^38 (the plans' floor divisions at the top of
+    their range)."""
     hi = (1 << bits) - 1
     cases = [dict(mult_rng=(1 << 12, 1 << 14), shift=8),
              dict(mult_rng=(1, 3), shift=0, clip=(1, hi - 1) if hi > 2 else (0, hi)),
              dict(mult_rng=(-(1 << 10), 1 << 10), shift=9),
-             dict(mult_rng=((1 << 30), (1 << 31) - 1), shift=40)]
+             dict(mult_rng=((1 << 30), (1 << 31) - 1), shift=40),
+             dict(mult_rng=(1, 1 << 8), shift=30),
+             dict(mult_rng=((1 << 29), (1 << 30)), shift=30),
+             dict(mult_rng=(1 << 20, 1 << 22), shift=24)]
     for j, kw in enumerate(cases):
         L = layer(bits, 3, 12, 14, 32, 3, 1, seed=50 + j, **kw)
         check(qnn, orc, L)
