@@ -467,12 +467,12 @@ struct PoolWin {
     }
 };
 
-template <int BITS, int P, int KH, int KW, int WOP, bool POOL, bool BAND, bool STAIR>
 // The leading scalar arguments repeat the fields of a that the first input
 // loads depend on (and the grid width): built with kernel-argument preloading,
 // they are in scalar registers when the waves start, so the first loads issue
 // without waiting for a scalar-load round trip (INT-4 batch-64 layer cold 6.76
 // -> 6.16 us, INT-8 batch-1 layer 4.87 -> 4.49 us, measured side by side).
+template <int BITS, int P, int KH, int KW, int WOP, bool POOL, bool BAND, bool STAIR>
 __global__ void __launch_bounds__(256) conv_img_kernel(const uint8_t *px, int32_t pngroups,
                                                        int32_t pbands, int32_t pbrows, int32_t ptrows, int32_t pph,
                                                        int32_t ph_, int32_t pw_, uint32_t pdbm, uint32_t pdbs,
